@@ -1,0 +1,269 @@
+"""Pins of the fp64 oracle against facts that do not come from the oracle.
+
+Each pin targets a plausible mistake: wrong bit order or packing axis (numpy's
+packbits, worked words), wrong sign decode (round trips, closed forms), a
+dropped or mis-scaled delta term or a transposed operand (exact brute force,
+one-hot rows, distributivity), wrong tenant routing (tenant invariants).
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import brute
+import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "pack_words.txt")
+
+
+def numpy_pack(plus: np.ndarray) -> np.ndarray:
+    """Library packer: numpy.packbits little-endian bit order, bytes -> '<u4'."""
+    rows, K = plus.shape
+    return np.packbits(plus.astype(np.uint8), axis=-1, bitorder="little").view("<u4").reshape(rows, K // 32)
+
+
+def numpy_signs(packed: np.ndarray, K: int) -> np.ndarray:
+    """Library decode: numpy.unpackbits little-endian -> +1/-1."""
+    bits = np.unpackbits(np.ascontiguousarray(packed).view(np.uint8), axis=-1,
+                         bitorder="little")[..., :K]
+    return bits.astype(np.float64) * 2.0 - 1.0
+
+
+def bf16(bits):
+    return wl.bf16_bits_to_f32(bits).astype(np.float64)
+
+
+# ---------------------------------------------------------------- pack / unpack
+
+def _parse_positions(spec, K):
+    if spec == "all":
+        return list(range(K))
+    if spec == "none":
+        return []
+    if spec == "even":
+        return list(range(0, K, 2))
+    if spec == "odd":
+        return list(range(1, K, 2))
+    out = []
+    for part in spec.split(","):
+        if "-" in part:
+            a, b = part.split("-")
+            out.extend(range(int(a), int(b) + 1))
+        else:
+            out.append(int(part))
+    return out
+
+
+def _golden_cases():
+    cases = []
+    with open(GOLDEN) as f:
+        for line in f:
+            line = line.strip()
+            if not line or line.startswith("#"):
+                continue
+            name, K, pos, words = [c.strip() for c in line.split("|")]
+            cases.append((name, int(K), pos, [int(w, 16) for w in words.split()]))
+    return cases
+
+
+@pytest.mark.parametrize("case", _golden_cases(), ids=lambda c: c[0])
+@pytest.mark.parametrize("dtype", ["f32", "i8", "bf16"])
+def test_pack_worked_words(case, dtype):
+    name, K, spec, words = case
+    plus = np.zeros(K, dtype=bool)
+    plus[_parse_positions(spec, K)] = True
+    s = np.where(plus, 1.0, -1.0).astype(np.float32)[None]
+    if dtype == "i8":
+        s = s.astype(np.int8)
+    elif dtype == "bf16":
+        s = wl.f32_to_bf16_bits(s)
+    got = oracle.pack(s)
+    assert [int(w) for w in got[0]] == words
+
+
+@pytest.mark.parametrize("rows,K", [(1, 32), (7, 96), (33, 256), (64, 4096)])
+def test_pack_equals_numpy_packbits(rows, K):
+    rng = np.random.default_rng(rows * 1000 + K)
+    plus = rng.random((rows, K)) < 0.5
+    ref = numpy_pack(plus)
+    f = np.where(plus, 1.0, -1.0).astype(np.float32)
+    np.testing.assert_array_equal(oracle.pack(f), ref)
+    np.testing.assert_array_equal(oracle.pack(f.astype(np.int8)), ref)
+    np.testing.assert_array_equal(oracle.pack(wl.f32_to_bf16_bits(f)), ref)
+
+
+def test_pack_special_values():
+    # bit = complement of the sign bit, whatever the magnitude
+    f = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, -np.nan, 1e-45, -1e-45,
+                  3.5, -3.5, 1e38, -1e38] + [1.0] * 20, dtype=np.float32)
+    signbit = np.signbit(f)
+    ref = numpy_pack(~signbit[None])
+    np.testing.assert_array_equal(oracle.pack(f[None]), ref)
+    i8 = np.arange(-128, 128, dtype=np.int16).astype(np.int8).reshape(8, 32)
+    np.testing.assert_array_equal(oracle.pack(i8), numpy_pack(i8 >= 0))
+    bits = np.arange(0, 65536, 2048, dtype=np.uint16)[None]  # 32 patterns
+    np.testing.assert_array_equal(oracle.pack(bits), numpy_pack((bits >> 15) == 0))
+
+
+def test_roundtrips():
+    rng = np.random.default_rng(5)
+    words = wl.uniform_words(rng, (17, 8))
+    signs = oracle.unpack(words, 256)
+    np.testing.assert_array_equal(signs, numpy_signs(words, 256))
+    np.testing.assert_array_equal(oracle.pack(signs.astype(np.float32)), words)
+    s = wl.random_signs_i8(rng, (9, 64))
+    np.testing.assert_array_equal(oracle.unpack(oracle.pack(s), 64), s.astype(np.float64))
+
+
+def test_pack_rejects_ragged_k():
+    with pytest.raises(ValueError):
+        oracle.pack(np.ones((2, 48), dtype=np.float32))
+
+
+# --------------------------------------------------------------------- matmul
+
+def _exact_vs_oracle(p: wl.Problem, rel=1e-15):
+    packed = p.packed if p.packed is not None else np.stack([oracle.pack(s) for s in p.signs])
+    exact = brute.matmul_exact(p.x.tolist(), p.w.tolist(), packed.tolist(), p.alpha.tolist(),
+                               None if p.tenant_ids is None else p.tenant_ids.tolist())
+    got = oracle.matmul(p.x, p.w, packed, p.alpha, p.tenant_ids)
+    for m in range(p.M):
+        for n in range(p.N):
+            e = exact[m][n]
+            if e is None:
+                assert np.isnan(got[m, n])
+                continue
+            err = abs(float(e - type(e)(got[m, n])))
+            scale = max(abs(float(e)), 1e-300)
+            # the fp64 sum of K products has error <= ~K*eps*sum|terms|; bound it by
+            # the row's absolute sum to stay meaningful under cancellation
+            absum = sum(abs(bf16(p.x[m, k])) * (abs(bf16(p.w[n, k])) + abs(float(p.alpha[0 if p.tenant_ids is None else p.tenant_ids[m]])))
+                        for k in range(p.K))
+            assert err <= rel * scale + 4 * p.K * 2.0 ** -53 * absum, (m, n, err, float(e))
+
+
+def test_brute_force_2x32x4():
+    p = wl.make_problem(2, 4, 32, 1, seed=11, y_dtype="f32")
+    _exact_vs_oracle(p)
+
+
+@pytest.mark.parametrize("M,N,K,T", [(1, 1, 32, 1), (3, 5, 64, 2), (4, 3, 96, 3)])
+def test_brute_force_random_tiny(M, N, K, T):
+    p = wl.make_problem(M, N, K, T, seed=M * 100 + N * 10 + K, multi_tenant=T > 1)
+    _exact_vs_oracle(p)
+
+
+def test_brute_force_tiny_int8_signs():
+    p = wl.make_problem(2, 6, 64, 1, seed=3, signs_as_int8=True)
+    _exact_vs_oracle(p)
+
+
+def test_brute_force_self_pins():
+    # the brute force's own bf16 decode and sign extraction against numpy
+    rng = np.random.default_rng(1)
+    bits = wl.normal_bf16(rng, (64,), 3.0)
+    for b in bits:
+        assert float(brute.bf16_bits_to_fraction(int(b))) == float(wl.bf16_bits_to_f32(np.array([b]))[0])
+    words = wl.uniform_words(rng, (2,))
+    ref = numpy_signs(words[None], 64)[0]
+    assert [brute.sign_from_words(words, k) for k in range(64)] == ref.tolist()
+
+
+def test_distributivity():
+    # x (W + a S)^T computed by numpy in fp64 with numpy's own sign decode
+    p = wl.make_problem(5, 37, 128, 1, seed=7)
+    S = numpy_signs(p.packed[0], p.K)
+    fused = bf16(p.x) @ (bf16(p.w) + np.float64(p.alpha[0]) * S).T
+    got = oracle.matmul(p.x, p.w, p.packed, p.alpha)
+    np.testing.assert_allclose(got, fused, rtol=1e-12, atol=1e-12 * np.abs(fused).max())
+
+
+def test_alpha_zero_is_plain_gemm():
+    p = wl.make_problem(6, 33, 256, 1, seed=8)
+    a0 = np.zeros(1, dtype=np.float32)
+    got = oracle.matmul(p.x, p.w, p.packed, a0)
+    ref = bf16(p.x) @ bf16(p.w).T
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-13 * np.abs(ref).max())
+
+
+def test_sign_flip_negates_delta_exactly():
+    p = wl.make_problem(3, 9, 160, 1, seed=9)
+    b1, d1, _ = oracle.matmul_parts(p.x, p.w, p.packed, p.alpha)
+    b2, d2, _ = oracle.matmul_parts(p.x, p.w, ~p.packed, p.alpha)
+    assert np.array_equal(d2, -d1)
+    assert np.array_equal(b1, b2)
+
+
+def test_closed_form_ones_row():
+    # x = 1, W = 0:  y[n] = alpha * (2 popcount(S[n]) - K), exactly
+    rng = np.random.default_rng(10)
+    K, N = 224, 19
+    words = wl.uniform_words(rng, (1, N, K // 32))
+    x = np.full((2, K), 0x3F80, dtype=np.uint16)         # bf16 1.0
+    w = np.zeros((N, K), dtype=np.uint16)
+    for a in (1.0, 2.0 ** -10, 7.25e-4):
+        alpha = np.array([a], dtype=np.float32)
+        y = oracle.matmul(x, w, words, alpha)
+        pc = np.array([sum(int(v).bit_count() for v in words[0, n]) for n in range(N)])
+        ref = np.float64(alpha[0]) * (2 * pc - K)
+        assert np.array_equal(y[0], ref) and np.array_equal(y[1], ref)
+
+
+def test_one_hot_rows_pick_weights_and_signs():
+    # x = e_k:  y[n] = W[n, k] + alpha * s[n, k] for every k (all bit positions, word edges)
+    p = wl.make_problem(1, 11, 96, 1, seed=12)
+    S = numpy_signs(p.packed[0], p.K)
+    x = np.zeros((p.K, p.K), dtype=np.uint16)
+    x[np.arange(p.K), np.arange(p.K)] = 0x3F80
+    y = oracle.matmul(x, p.w, p.packed, p.alpha)           # [K, N]
+    ref = bf16(p.w).T + np.float64(p.alpha[0]) * S.T
+    assert np.array_equal(y, ref)
+
+
+def test_tenant_routing_invariants():
+    rng = np.random.default_rng(13)
+    M, N, K, T = 12, 7, 64, 4
+    p = wl.make_problem(M, N, K, T, seed=14, multi_tenant=True)
+    y = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids)
+    # each row equals the single-tenant result of its own tenant
+    for m in range(M):
+        t = p.tenant_ids[m]
+        ys = oracle.matmul(p.x[m:m + 1], p.w, p.packed[t], p.alpha[t:t + 1])
+        assert np.array_equal(y[m], ys[0])
+    # permuting rows together with their tenant ids permutes the output
+    perm = rng.permutation(M)
+    yp = oracle.matmul(p.x[perm], p.w, p.packed, p.alpha, p.tenant_ids[perm])
+    assert np.array_equal(yp, y[perm])
+    # identical tenants == one tenant
+    same = np.repeat(p.packed[:1], T, axis=0)
+    a_same = np.repeat(p.alpha[:1], T)
+    y1 = oracle.matmul(p.x, p.w, same, a_same, p.tenant_ids)
+    y0 = oracle.matmul(p.x, p.w, p.packed[:1], p.alpha[:1])
+    assert np.array_equal(y1, y0)
+    # out-of-range tenant ids give NaN rows, other rows unaffected
+    bad = p.tenant_ids.copy()
+    bad[3], bad[5] = -1, T
+    yb = oracle.matmul(p.x, p.w, p.packed, p.alpha, bad)
+    assert np.all(np.isnan(yb[[3, 5]]))
+    keep = [m for m in range(M) if m not in (3, 5)]
+    assert np.array_equal(yb[keep], y[keep])
+
+
+def test_sampled_columns_match_full():
+    p = wl.make_problem(4, 50, 64, 2, seed=15, multi_tenant=True)
+    full = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids)
+    idx = np.array([49, 0, 17, 17, 3])
+    part = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids, n_idx=idx)
+    assert np.array_equal(part, full[:, idx])
+
+
+def test_empty_shapes():
+    x = np.zeros((0, 64), dtype=np.uint16)
+    w = np.zeros((5, 64), dtype=np.uint16)
+    y = oracle.matmul(x, w, np.zeros((1, 5, 2), np.uint32), np.ones(1, np.float32))
+    assert y.shape == (0, 5)
+    # K = 0: every sum is empty, so y = 0
+    y = oracle.matmul(np.zeros((2, 0), np.uint16), np.zeros((3, 0), np.uint16),
+                      np.zeros((1, 3, 0), np.uint32), np.ones(1, np.float32))
+    assert np.array_equal(y, np.zeros((2, 3)))
