@@ -1,0 +1,303 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X binary-delta matmul.
+
+Prints ONE JSON line.  Headline workload (one "step"): the single-tenant
+decode GEMV pair x[1,4096] and x[16,4096] against W_base[4096,4096] with one
+packed 4096x4096 sign matrix, bf16 output -- two launches of the decode kernel.
+`value` is whole-step HBM throughput in TB/s from algorithmic bytes (W_base +
+packed signs + x + y per launch) over the HIP-event time of exactly `--steps`
+steps, with all inputs resident in HBM.
+
+Cache defeat: every launch reads its own (W_base, signs) buffer set; sets rotate
+over more than twice the 256 MB Infinity Cache, so each launch streams its
+operands from HBM.  Steps are replayed from a HIP graph (captured once) so host
+launch overhead does not pace the GPU.
+
+Also reported (same run): the other workloads' throughput (multi-tenant decode,
+prefill, LLaMA-7B-shaped 32-layer sweep) under "workloads", the dominant
+kernel's roofline fraction, and the fp64 CPU oracle timed on a bounded sample
+of the headline workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "binary-delta matmul TB/s (decode) & TFLOP/s (prefill), % of MI355X roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak, published
+MALL_BYTES = 256 << 20
+
+
+def algorithmic_bytes(M, N, K, tenants_used, y_bytes=2):
+    """W_base + packed signs of the tenants read + x + y (alpha and ids: negligible)."""
+    return N * K * 2 + tenants_used * N * (K // 32) * 4 + M * K * 2 + M * N * y_bytes
+
+
+class Launcher:
+    """Pre-marshalled C-ABI calls: each call() only passes stored pointers and the
+    current stream to bitdelta_matmul (nothing else runs per call)."""
+
+    def __init__(self, lib):
+        self.lib = lib
+
+    def matmul(self, x, w, packed, alpha, tid, y):
+        import ctypes
+        import torch
+        import paper_2609_36800_amd as bd
+        M, K = x.shape
+        N = w.shape[0]
+        T = alpha.numel()
+        args = (x.data_ptr(), M, K, w.data_ptr(), N, packed.data_ptr(), alpha.data_ptr(),
+                None if tid is None else tid.data_ptr(), T, y.data_ptr(), bd.BF16, bd.PATH_AUTO)
+        f = self.lib.bitdelta_matmul_with_path
+
+        def call():
+            rc = f(*args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"bitdelta_matmul failed: {rc}")
+        return call
+
+
+def make_sets(count, M, N, K, T, multi, seed, dev):
+    import workloads as wl
+    sets = []
+    for i in range(count):
+        d = wl.device_problem(M, N, K, T, multi_tenant=multi, seed=seed + i, device=dev)
+        sets.append(d)
+    return sets
+
+
+def capture(calls, warmup_calls):
+    """Run warmup_calls eagerly, then capture `calls` once into a HIP graph
+    (falls back to eager replay if capture is unavailable)."""
+    import torch
+    for c in warmup_calls:
+        c()
+    torch.cuda.synchronize()
+    try:
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            g.capture_begin()
+            for c in calls:
+                c()
+            g.capture_end()
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        return g.replay, True, g
+    except Exception as e:  # graph capture unavailable: replay eagerly
+        print(f"# graph capture failed ({e}); timing eager launches", file=sys.stderr)
+
+        def eager():
+            for c in calls:
+                c()
+        return eager, False, None
+
+
+def timed(replay, reps):
+    import torch
+    torch.cuda.synchronize()
+    st = torch.cuda.Event(enable_timing=True)
+    en = torch.cuda.Event(enable_timing=True)
+    st.record()
+    for _ in range(reps):
+        replay()
+    en.record()
+    torch.cuda.synchronize()
+    return st.elapsed_time(en) / 1e3  # seconds
+
+
+def bench_workload(name, shapes, T, multi, flops_fn, steps, warmup, dev, launcher, seed,
+                   rotate=True):
+    """Time exactly `steps` steps; a step is one launch per (M, N, K) in `shapes`.
+
+    With rotate, consecutive launches read different buffer sets and the sets
+    total more than twice the Infinity Cache.  The `steps` steps are captured
+    into one graph and replayed once inside the timed region.
+    """
+    import numpy as np
+    import torch
+    est = sum(algorithmic_bytes(M, N, K, T) for (M, N, K) in shapes)
+    nrot = max(2, -(-2 * MALL_BYTES // est)) if rotate else 1
+    rot_calls, keep, rot_bytes = [], [], []
+    for r in range(nrot):
+        step_calls, b = [], 0
+        for j, (M, N, K) in enumerate(shapes):
+            d = make_sets(1, M, N, K, T, multi, seed + 1000 * j + r, dev)[0]
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            used = 1 if d["tenant_ids"] is None else len(np.unique(d["tenant_ids"].cpu().numpy()))
+            b += algorithmic_bytes(M, N, K, used)
+            keep.append((d, y))
+            step_calls.append(launcher.matmul(d["x"], d["w"], d["packed"], d["alpha"],
+                                              d["tenant_ids"], y))
+        rot_calls.append(step_calls)
+        rot_bytes.append(b)
+    calls = [c for i in range(steps) for c in rot_calls[i % nrot]]
+    warm = [c for i in range(max(1, warmup)) for c in rot_calls[i % nrot]]
+    replay, graphed, graph = capture(calls, warm)
+    secs = timed(replay, 1)
+    total_bytes = sum(rot_bytes[i % nrot] for i in range(steps))
+    sec_per_step = secs / steps
+    flops = sum(flops_fn(*s) for s in shapes)
+    res = {
+        "workload": name, "steps": steps, "graphed": graphed, "buffer_sets": nrot * len(shapes),
+        "ms_per_step": sec_per_step * 1e3, "bytes_per_step": total_bytes / steps,
+        "TBps": total_bytes / secs / 1e12,
+        "TFLOPs": flops * steps / secs / 1e12,
+        "launches_per_step": len(shapes),
+        "avg_launch_us": secs / (steps * len(shapes)) * 1e6,
+    }
+    del keep, calls, warm, rot_calls, graph
+    torch.cuda.empty_cache()
+    return res
+
+
+def llama_sweep(dev, launcher, warmup):
+    """32 layers x 7 matrices, 8 tenants, 64 rows: one pass over ~19.7 GB."""
+    import torch
+    import workloads as wl
+    import numpy as np
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    M, T = wl.LLAMA_ROWS, wl.LLAMA_TENANTS
+    x4096 = torch.randn((M, 4096), generator=g, device=dev).to(torch.bfloat16)
+    x11008 = torch.randn((M, 11008), generator=g, device=dev).to(torch.bfloat16)
+    tid = torch.randint(0, T, (M,), generator=g, device=dev, dtype=torch.int32)
+    used = len(np.unique(tid.cpu().numpy()))
+    calls, per_matrix = [], {}
+    keep = []
+    total_bytes = 0
+    for layer in range(wl.LLAMA_LAYERS):
+        for idx, (name, N, K) in enumerate(wl.LLAMA_MATRICES):
+            w = (torch.randn((N, K), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+            pk = torch.randint(0, 256, (T, N, K // 32, 4), generator=g, device=dev,
+                               dtype=torch.uint8).view(torch.int32).reshape(T, N, K // 32)
+            a = torch.rand((T,), generator=g, device=dev) * 9e-4 + 1e-4
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            x = x4096 if K == 4096 else x11008
+            keep.append((w, pk, a, y))
+            calls.append(launcher.matmul(x, w, pk, a, tid, y))
+            b = algorithmic_bytes(M, N, K, used)
+            per_matrix.setdefault(name, {"N": N, "K": K, "bytes": b})
+            total_bytes += b
+    replay, graphed, graph = capture(calls, calls)
+    secs = timed(replay, 3) / 3
+    # per-matrix-type time: time each type's 32 launches on its own
+    for name in per_matrix:
+        idxs = [i for i, c in enumerate(calls) if wl.LLAMA_MATRICES[i % 7][0] == name]
+        sub = [calls[i] for i in idxs]
+        r, _, g2 = capture(sub, sub)
+        t = timed(r, 3) / 3 / len(sub)
+        del g2
+        per_matrix[name]["us"] = t * 1e6
+        per_matrix[name]["TBps"] = per_matrix[name]["bytes"] / t / 1e12
+    del keep, calls, graph
+    torch.cuda.empty_cache()
+    return {"workload": "LLaMA-7B-shaped sweep: 32 layers x {q,k,v,o,gate,up,down}, 8 tenants, "
+                        "64 rows", "graphed": graphed, "tenants_used": used,
+            "ms_per_pass": secs * 1e3, "bytes_per_pass": total_bytes,
+            "TBps": total_bytes / secs / 1e12, "per_matrix": per_matrix}
+
+
+def cpu_baseline(budget_s: float):
+    """fp64 oracle timed on the headline workload (the M = 1 and M = 16 pair
+    against one 4096x4096 matrix), repeated until about budget_s seconds."""
+    import oracle
+    import workloads as wl
+    p1 = wl.decode(1, seed=0)
+    p16 = wl.make_problem(16, 4096, 4096, 1, seed=0)
+    p16.w, p16.packed, p16.alpha = p1.w, p1.packed, p1.alpha
+    b = algorithmic_bytes(1, 4096, 4096, 1) + algorithmic_bytes(16, 4096, 4096, 1)
+    reps, secs = 0, 0.0
+    while secs < budget_s and reps < 1000:
+        t0 = time.perf_counter()
+        oracle.matmul(p1.x, p1.w, p1.packed, p1.alpha)
+        oracle.matmul(p16.x, p16.w, p16.packed, p16.alpha)
+        secs += time.perf_counter() - t0
+        reps += 1
+    return {"value": reps * b / secs / 1e12, "unit": "TB/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"full decode pair (M=1 and M=16, N=K=4096, {b} algorithmic bytes per "
+                      f"pass), {reps} passes in {secs:.2f} s, fp64 with OpenMP over features",
+            "seconds": secs}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--only-headline", action="store_true", help="skip the other workloads")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-budget", type=float, default=10.0)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(the operator would shard along output features with no exchange).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_36800_amd as bd
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    launcher = Launcher(bd.load_library())
+
+    head = bench_workload(
+        "single-tenant decode GEMV pair: x 1x4096 and 16x4096, W_base 4096x4096, "
+        "one packed 4096x4096 sign matrix, bf16 out",
+        [(1, 4096, 4096), (16, 4096, 4096)], 1, False, lambda M, N, K: 2 * M * N * K,
+        args.steps, args.warmup, dev, launcher, seed=1)
+
+    avg_launch_s = head["avg_launch_us"] / 1e6
+    per_launch_bytes = head["bytes_per_step"] / head["launches_per_step"]
+    achieved = per_launch_bytes / avg_launch_s / 1e9
+    roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                "kernel": "skinny_single_kernel (M<=16: one 16-row block)",
+                "per_launch_bytes": per_launch_bytes,
+                "avg_launch_us": head["avg_launch_us"]}
+
+    workloads = [head]
+    if not args.only_headline:
+        workloads.append(bench_workload(
+            "multi-tenant decode: x 32x4096 (tenant id per row, 16 tenants), W_base 11008x4096",
+            [(32, 11008, 4096)], 16, True, lambda M, N, K: 2 * M * N * K,
+            100, args.warmup, dev, launcher, seed=50))
+        pf = bench_workload(
+            "prefill: x 4096x4096, W_base 4096x4096, one tenant, fused bf16 GEMM",
+            [(4096, 4096, 4096)], 1, False, lambda M, N, K: 2 * M * N * K,
+            20, args.warmup, dev, launcher, seed=90, rotate=False)
+        pf["mfma_frac"] = pf["TFLOPs"] / BF16_PEAK_TFLOPS
+        workloads.append(pf)
+        workloads.append(llama_sweep(dev, launcher, args.warmup))
+
+    cpu = None if args.no_cpu else cpu_baseline(args.cpu_budget)
+
+    out = {
+        "metric": METRIC, "value": head["TBps"], "unit": "TB/s", "n_gpus": 1,
+        "steps": head["steps"], "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": head["workload"], "global_batch": 17, "K": 4096, "N": 4096,
+                   "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "workloads": workloads,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

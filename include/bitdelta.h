@@ -1,0 +1,142 @@
+/*
+ * bitdelta.h -- C ABI of the MI355X (gfx950) binary-delta matmul library.
+ *
+ * The operator is the BitDelta GEMM that the paper evaluates as a "standard"
+ * and a "batched" kernel (Section 4.4; kernel description in Appendix A.2,
+ * "BitDelta" paragraph): a fine-tuned weight is a shared base weight plus a
+ * per-tenant scale times a matrix of signs stored one bit per weight,
+ *
+ *     y[m][n] = sum_k x[m][k] * W_base[n][k]
+ *             + alpha[t] * sum_k x[m][k] * s_t[n][k],     t = tenant of row m,
+ *
+ * with the sign decoded from its packed bit b as s = 2b - 1 (Appendix A.2).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All array arguments are DEVICE pointers owned by the caller; the library
+ *    never allocates, frees or retains them, keeps no global state, and is
+ *    re-entrant.  Arrays are dense and row-major.
+ *  - Work is enqueued asynchronously on `stream` (0 = the null stream); the
+ *    functions return once the kernels are launched.
+ *  - Arguments are checked on the host before anything is launched; a
+ *    negative status means nothing was enqueued and no memory was touched.
+ *  - Packed sign layout: uint32 words [rows][K/32]; bit i (LSB = bit 0) of word
+ *    j of a row holds element k = 32*j + i; bit 1 means +1, bit 0 means -1.
+ *    K must be a multiple of 32, so no word is partially used.
+ *  - bf16 data is passed as its 16-bit patterns (uint16_t).
+ *  - Paths are deterministic: the same inputs give bitwise-identical outputs.
+ */
+#ifndef BITDELTA_H
+#define BITDELTA_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    BITDELTA_OK = 0,
+    BITDELTA_ERR_NULL = -1,        /* a required pointer is NULL                 */
+    BITDELTA_ERR_SHAPE = -2,       /* negative size, K % 32 != 0, T < 1, ...     */
+    BITDELTA_ERR_ALIGN = -3,       /* a pointer is not aligned as required       */
+    BITDELTA_ERR_DTYPE = -4,       /* dtype code not accepted by this argument   */
+    BITDELTA_ERR_UNSUPPORTED = -5, /* valid request this path cannot serve       */
+    BITDELTA_ERR_HIP = -6,         /* the HIP runtime reported a launch failure  */
+    BITDELTA_ERR_ALIAS = -7        /* the output overlaps an input               */
+} bitdelta_status;
+
+typedef enum {
+    BITDELTA_F32 = 0,   /* IEEE binary32                  */
+    BITDELTA_BF16 = 1,  /* bfloat16 bit patterns          */
+    BITDELTA_I8 = 2     /* signed 8-bit integers          */
+} bitdelta_dtype;
+
+/* Kernel paths of bitdelta_matmul (see bitdelta_matmul_path). */
+typedef enum {
+    BITDELTA_PATH_AUTO = 0,
+    BITDELTA_PATH_SKINNY = 1,   /* M <= 64, any tenants: HBM-bound decode path   */
+    BITDELTA_PATH_PREFILL = 2   /* one tenant, any M: fused (W + alpha*s) GEMM   */
+} bitdelta_path;
+
+/*
+ * Pack signs into bits (the storage format of the binary delta, Appendix A.2).
+ *
+ *   signs     [rows][K] of in_dtype (F32, BF16 or I8); alignment 4 * element size
+ *   packed    [rows][K/32] uint32, 4-byte aligned
+ *
+ * Bit = 1 exactly when the element's sign bit is clear: +1 -> 1, -1 -> 0, and
+ * for other values +0/+inf/positive NaN -> 1, -0/-inf/negative NaN -> 0,
+ * int8 v >= 0 -> 1.  rows == 0 or K == 0 is a no-op.
+ * Errors: NULL, SHAPE (rows < 0, K < 0, K % 32), ALIGN, DTYPE, HIP.
+ */
+int bitdelta_pack(const void* signs, int in_dtype, int64_t rows, int64_t K,
+                  uint32_t* packed, hipStream_t stream);
+
+/*
+ * Decode packed bits into +1 / -1 (s = 2b - 1, Appendix A.2).
+ *
+ *   packed    [rows][K/32] uint32, 4-byte aligned
+ *   signs     [rows][K] of out_dtype (F32, BF16 or I8); alignment 4 * element size
+ *
+ * Errors: NULL, SHAPE, ALIGN, DTYPE, HIP.
+ */
+int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K,
+                    void* signs, int out_dtype, hipStream_t stream);
+
+/*
+ * Binary-delta matmul, standard and batched (multi-tenant) forms (Section 4.4).
+ *
+ *   x           [M][K] bf16, 16-byte aligned
+ *   w_base      [N][K] bf16, 16-byte aligned
+ *   packed_s    [T][N][K/32] uint32 sign bits, 4-byte aligned
+ *   alpha       [T] fp32 scales (device memory), 4-byte aligned
+ *   tenant_ids  [M] int32 (device memory): row m uses tenant tenant_ids[m];
+ *               NULL means every row uses tenant 0 (the standard form)
+ *   T           number of tenants held in packed_s / alpha, >= 1
+ *   y           [M][N] of y_dtype (F32 or BF16), 16-byte aligned; must not
+ *               overlap any input
+ *
+ * Accumulation is fp32; a bf16 output is rounded to nearest-even once at the
+ * end.  The single-tenant path for M > 64 rounds the effective weight
+ * W_base + alpha*s to bf16 before its one matrix-core GEMM; the M <= 64 path
+ * keeps the two sums apart and never rounds the weight.
+ * A row whose tenant id is outside [0, T) is written as quiet NaN (ids live in
+ * device memory, so they are not checked on the host).
+ * M == 0 or N == 0 is a no-op; K == 0 writes zeros.
+ * Multi-tenant requests with M > 64 are served 64 rows at a time.
+ * Errors: NULL, SHAPE, ALIGN, DTYPE, ALIAS, HIP.
+ */
+int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K,
+                    const uint16_t* w_base, int64_t N,
+                    const uint32_t* packed_s, const float* alpha,
+                    const int32_t* tenant_ids, int32_t T,
+                    void* y, int y_dtype, hipStream_t stream);
+
+/*
+ * Same as bitdelta_matmul with the kernel path chosen by the caller (tests
+ * exercise each path on the same inputs).  BITDELTA_PATH_PREFILL with
+ * tenant_ids != NULL returns BITDELTA_ERR_UNSUPPORTED; BITDELTA_PATH_SKINNY
+ * accepts any M (64 rows per launch).
+ */
+int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K,
+                              const uint16_t* w_base, int64_t N,
+                              const uint32_t* packed_s, const float* alpha,
+                              const int32_t* tenant_ids, int32_t T,
+                              void* y, int y_dtype, int path, hipStream_t stream);
+
+/* The path bitdelta_matmul picks for these sizes (no side effects). */
+int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids);
+
+/* Static, NUL-terminated description of a status code. */
+const char* bitdelta_status_string(int status);
+
+/* Library ABI version (major * 100 + minor). */
+int bitdelta_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BITDELTA_H */

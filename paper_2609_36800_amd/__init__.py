@@ -1,0 +1,171 @@
+"""Python binding of the MI355X binary-delta matmul library (``libbitdelta.so``).
+
+Argument marshalling only: every step of the operator runs in the gfx950 HIP
+kernels behind the C ABI of ``include/bitdelta.h``.  PyTorch provides device
+memory and the current stream.  There is no fallback: if the library is not
+built, importing works but every call raises.
+
+    pack(signs)                          -> int32 [rows, K/32] packed sign words
+    unpack(packed, K, dtype)             -> [rows, K] of +1 / -1
+    matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=bf16) -> y
+
+The operator (the standard and batched BitDelta GEMMs, Section 4.4 of the
+paper) is  y[m, n] = sum_k x[m, k] W[n, k] + alpha[t] sum_k x[m, k] s_t[n, k],
+with s = 2b - 1 decoded from the packed bits (Appendix A.2).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libbitdelta.so")
+
+OK = 0
+F32, BF16, I8 = 0, 1, 2
+PATH_AUTO, PATH_SKINNY, PATH_PREFILL = 0, 1, 2
+
+EXPORTED = (
+    "bitdelta_pack",
+    "bitdelta_unpack",
+    "bitdelta_matmul",
+    "bitdelta_matmul_with_path",
+    "bitdelta_matmul_path",
+    "bitdelta_status_string",
+    "bitdelta_version",
+)
+
+_lib = None
+
+
+class BitDeltaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"bitdelta status {status}: {msg}")
+        self.status = status
+
+
+def load_library(path: str = LIB_PATH):
+    """Load ``libbitdelta.so`` (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build the HIP library first "
+            "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    P, I64, I32, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
+    lib.bitdelta_pack.argtypes = [P, I, I64, I64, P, P]
+    lib.bitdelta_pack.restype = I
+    lib.bitdelta_unpack.argtypes = [P, I64, I64, P, I, P]
+    lib.bitdelta_unpack.restype = I
+    lib.bitdelta_matmul.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, P]
+    lib.bitdelta_matmul.restype = I
+    lib.bitdelta_matmul_with_path.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, I, P]
+    lib.bitdelta_matmul_with_path.restype = I
+    lib.bitdelta_matmul_path.argtypes = [I64, I64, I64, I32, I]
+    lib.bitdelta_matmul_path.restype = I
+    lib.bitdelta_status_string.argtypes = [I]
+    lib.bitdelta_status_string.restype = ctypes.c_char_p
+    lib.bitdelta_version.argtypes = []
+    lib.bitdelta_version.restype = I
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().bitdelta_status_string(status).decode()
+
+
+def _check(status: int):
+    if status != OK:
+        raise BitDeltaError(status, status_string(status))
+
+
+def _stream(t):
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _dtype_code(dt):
+    import torch
+    codes = {torch.float32: F32, torch.bfloat16: BF16, torch.int8: I8}
+    if dt not in codes:
+        raise TypeError(f"unsupported dtype {dt}")
+    return codes[dt]
+
+
+def _dev(t, name, dtypes):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def pack(signs, out=None):
+    """Pack signs [rows, K] (float32 / bfloat16 / int8) into int32 words [rows, K/32]."""
+    import torch
+    _dev(signs, "signs", (torch.float32, torch.bfloat16, torch.int8))
+    rows, K = signs.shape
+    if out is None:
+        out = torch.empty((rows, K // 32), dtype=torch.int32, device=signs.device)
+    _dev(out, "out", (torch.int32,))
+    _check(load_library().bitdelta_pack(signs.data_ptr(), _dtype_code(signs.dtype), rows, K,
+                                        out.data_ptr(), _stream(signs)))
+    return out
+
+
+def unpack(packed, K: int, dtype=None, out=None):
+    """Decode int32 words [rows, K/32] into [rows, K] of +1 / -1 (float32 by default)."""
+    import torch
+    dtype = dtype or torch.float32
+    _dev(packed, "packed", (torch.int32,))
+    rows = packed.shape[0]
+    if out is None:
+        out = torch.empty((rows, K), dtype=dtype, device=packed.device)
+    _dev(out, "out", (torch.float32, torch.bfloat16, torch.int8))
+    _check(load_library().bitdelta_unpack(packed.data_ptr(), rows, K, out.data_ptr(),
+                                          _dtype_code(out.dtype), _stream(packed)))
+    return out
+
+
+def matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=None, out=None,
+           path: int = PATH_AUTO):
+    """y = x W^T + alpha_t x S_t^T.
+
+    x [M, K] bf16, w_base [N, K] bf16, packed_s int32 [T, N, K/32] (or [N, K/32]),
+    alpha fp32 [T], tenant_ids int32 [M] or None, out_dtype float32 or bfloat16.
+    """
+    import torch
+    out_dtype = out_dtype or torch.bfloat16
+    _dev(x, "x", (torch.bfloat16,))
+    _dev(w_base, "w_base", (torch.bfloat16,))
+    _dev(packed_s, "packed_s", (torch.int32,))
+    _dev(alpha, "alpha", (torch.float32,))
+    M, K = x.shape
+    N = w_base.shape[0]
+    T = alpha.numel()
+    if packed_s.dim() == 2:
+        packed_s = packed_s.unsqueeze(0)
+    if tuple(packed_s.shape) != (T, N, K // 32) or w_base.shape[1] != K:
+        raise ValueError(f"shape mismatch: x {tuple(x.shape)}, w {tuple(w_base.shape)}, "
+                         f"packed {tuple(packed_s.shape)}, alpha {T}")
+    tptr = None
+    if tenant_ids is not None:
+        _dev(tenant_ids, "tenant_ids", (torch.int32,))
+        if tenant_ids.numel() != M:
+            raise ValueError("tenant_ids needs one entry per row")
+        tptr = tenant_ids.data_ptr()
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=x.device)
+    _dev(out, "out", (torch.float32, torch.bfloat16))
+    _check(load_library().bitdelta_matmul_with_path(
+        x.data_ptr(), M, K, w_base.data_ptr(), N, packed_s.data_ptr(), alpha.data_ptr(),
+        tptr, T, out.data_ptr(), _dtype_code(out.dtype), path, _stream(x)))
+    return out
+
+
+def matmul_path(M: int, N: int, K: int, T: int, multi_tenant: bool) -> int:
+    return load_library().bitdelta_matmul_path(M, N, K, T, int(bool(multi_tenant)))

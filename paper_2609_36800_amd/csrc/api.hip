@@ -1,0 +1,150 @@
+// C ABI of the binary-delta matmul library: argument checks, path choice and
+// kernel launches.  Everything here runs on the host; nothing is allocated.
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "../../include/bitdelta.h"
+#include "internal.h"
+
+namespace {
+
+constexpr int kSkinnyRows = 64;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+int elem_size(int dtype) {
+    switch (dtype) {
+        case BITDELTA_F32: return 4;
+        case BITDELTA_BF16: return 2;
+        case BITDELTA_I8: return 1;
+        default: return 0;
+    }
+}
+
+bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
+    if (a == nullptr || b == nullptr || abytes == 0 || bbytes == 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? BITDELTA_OK : BITDELTA_ERR_HIP; }
+
+// Largest extent any kernel indexes with 32-bit arithmetic.
+constexpr int64_t kMaxDim = (int64_t)1 << 30;
+
+int check_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w, int64_t N,
+                 const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
+                 int32_t T, void* y, int y_dtype) {
+    if (M < 0 || N < 0 || K < 0 || T < 1) return BITDELTA_ERR_SHAPE;
+    if (K % 32 != 0) return BITDELTA_ERR_SHAPE;
+    if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return BITDELTA_ERR_SHAPE;
+    if (y_dtype != BITDELTA_F32 && y_dtype != BITDELTA_BF16) return BITDELTA_ERR_DTYPE;
+    if (M == 0 || N == 0) return BITDELTA_OK;
+    if (y == nullptr || alpha == nullptr) return BITDELTA_ERR_NULL;
+    if (K > 0 && (x == nullptr || w == nullptr || packed == nullptr)) return BITDELTA_ERR_NULL;
+    if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y, 16)) return BITDELTA_ERR_ALIGN;
+    if (!aligned(packed, 4) || !aligned(alpha, 4) || !aligned(tenant_ids, 4)) return BITDELTA_ERR_ALIGN;
+    const size_t ybytes = (size_t)M * (size_t)N * (size_t)elem_size(y_dtype);
+    if (overlaps(y, ybytes, x, (size_t)M * K * 2) || overlaps(y, ybytes, w, (size_t)N * K * 2) ||
+        overlaps(y, ybytes, packed, (size_t)T * N * (K / 32) * 4) ||
+        overlaps(y, ybytes, alpha, (size_t)T * 4) ||
+        overlaps(y, ybytes, tenant_ids, tenant_ids ? (size_t)M * 4 : 0))
+        return BITDELTA_ERR_ALIAS;
+    return BITDELTA_OK;
+}
+
+int choose_path(int64_t M, int has_tenant_ids) {
+    if (has_tenant_ids || M <= kSkinnyRows) return BITDELTA_PATH_SKINNY;
+    return BITDELTA_PATH_PREFILL;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bitdelta_version(void) { return 100; }
+
+const char* bitdelta_status_string(int status) {
+    switch (status) {
+        case BITDELTA_OK: return "ok";
+        case BITDELTA_ERR_NULL: return "a required pointer is NULL";
+        case BITDELTA_ERR_SHAPE: return "invalid shape (negative size, K not a multiple of 32, T < 1 or size too large)";
+        case BITDELTA_ERR_ALIGN: return "pointer not aligned as required";
+        case BITDELTA_ERR_DTYPE: return "dtype not accepted for this argument";
+        case BITDELTA_ERR_UNSUPPORTED: return "request not supported by the selected path";
+        case BITDELTA_ERR_HIP: return "HIP runtime error at launch";
+        case BITDELTA_ERR_ALIAS: return "output overlaps an input";
+        default: return "unknown status";
+    }
+}
+
+int bitdelta_pack(const void* signs, int in_dtype, int64_t rows, int64_t K, uint32_t* packed,
+                  hipStream_t stream) {
+    const int es = elem_size(in_dtype);
+    if (es == 0) return BITDELTA_ERR_DTYPE;
+    if (rows < 0 || K < 0 || K % 32 != 0) return BITDELTA_ERR_SHAPE;
+    if (rows == 0 || K == 0) return BITDELTA_OK;
+    if (signs == nullptr || packed == nullptr) return BITDELTA_ERR_NULL;
+    if (!aligned(signs, 4 * es) || !aligned(packed, 4)) return BITDELTA_ERR_ALIGN;
+    if (overlaps(packed, (size_t)rows * (K / 32) * 4, signs, (size_t)rows * K * es))
+        return BITDELTA_ERR_ALIAS;
+    return hip_status(bitdelta::launch_pack(signs, in_dtype, rows * K, packed, stream));
+}
+
+int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K, void* signs, int out_dtype,
+                    hipStream_t stream) {
+    const int es = elem_size(out_dtype);
+    if (es == 0) return BITDELTA_ERR_DTYPE;
+    if (rows < 0 || K < 0 || K % 32 != 0) return BITDELTA_ERR_SHAPE;
+    if (rows == 0 || K == 0) return BITDELTA_OK;
+    if (signs == nullptr || packed == nullptr) return BITDELTA_ERR_NULL;
+    if (!aligned(signs, 4 * es) || !aligned(packed, 4)) return BITDELTA_ERR_ALIGN;
+    if (overlaps(packed, (size_t)rows * (K / 32) * 4, signs, (size_t)rows * K * es))
+        return BITDELTA_ERR_ALIAS;
+    return hip_status(bitdelta::launch_unpack(packed, rows * K, signs, out_dtype, stream));
+}
+
+int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
+    (void)N;
+    (void)K;
+    (void)T;
+    return choose_path(M, has_tenant_ids);
+}
+
+int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
+                              int64_t N, const uint32_t* packed_s, const float* alpha,
+                              const int32_t* tenant_ids, int32_t T, void* y, int y_dtype,
+                              int path, hipStream_t stream) {
+    int rc = check_matmul(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, y, y_dtype);
+    if (rc != BITDELTA_OK) return rc;
+    if (path == BITDELTA_PATH_AUTO) path = choose_path(M, tenant_ids != nullptr);
+    if (path != BITDELTA_PATH_SKINNY && path != BITDELTA_PATH_PREFILL) return BITDELTA_ERR_UNSUPPORTED;
+    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr) return BITDELTA_ERR_UNSUPPORTED;
+    if (M == 0 || N == 0) return BITDELTA_OK;
+
+    if (path == BITDELTA_PATH_PREFILL)
+        return hip_status(bitdelta::launch_prefill(x, (int)M, (int)K, w_base, (int)N, packed_s,
+                                                   alpha, y, y_dtype, stream));
+
+    // Skinny path: 64 rows per launch (each launch streams W once more).
+    const int es = elem_size(y_dtype);
+    for (int64_t r0 = 0; r0 < M; r0 += kSkinnyRows) {
+        const int rows = (int)(M - r0 < kSkinnyRows ? M - r0 : kSkinnyRows);
+        rc = hip_status(bitdelta::launch_skinny(
+            x + r0 * K, rows, (int)K, w_base, (int)N, packed_s, alpha,
+            tenant_ids ? tenant_ids + r0 : nullptr, (int)T,
+            static_cast<char*>(y) + r0 * N * es, y_dtype, stream));
+        if (rc != BITDELTA_OK) return rc;
+    }
+    return BITDELTA_OK;
+}
+
+int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base, int64_t N,
+                    const uint32_t* packed_s, const float* alpha, const int32_t* tenant_ids,
+                    int32_t T, void* y, int y_dtype, hipStream_t stream) {
+    return bitdelta_matmul_with_path(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, y,
+                                     y_dtype, BITDELTA_PATH_AUTO, stream);
+}
+
+}  // extern "C"

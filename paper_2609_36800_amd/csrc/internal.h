@@ -1,0 +1,33 @@
+// Host-side launchers of the gfx950 kernels (one translation unit each).
+// Arguments are validated by the C-ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bitdelta {
+
+// Element dtype codes (same values as the public bitdelta_dtype).
+constexpr int kF32 = 0;
+constexpr int kBF16 = 1;
+constexpr int kI8 = 2;
+
+// Pack / unpack over a flat run of `elems` elements (a multiple of 32): the
+// packed words of consecutive rows are contiguous, so rows need no special care.
+hipError_t launch_pack(const void* signs, int dtype, int64_t elems, uint32_t* packed,
+                       hipStream_t stream);
+hipError_t launch_unpack(const uint32_t* packed, int64_t elems, void* signs, int dtype,
+                         hipStream_t stream);
+
+// Decode-shaped matmul for at most 64 rows (any number of tenants).
+hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                         const uint32_t* packed, const float* alpha,
+                         const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                         hipStream_t stream);
+
+// Prefill-shaped single-tenant matmul: one bf16 GEMM over W + alpha*s.
+hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
+                          hipStream_t stream);
+
+}  // namespace bitdelta

@@ -1,0 +1,139 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_36800_amd as bd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bitdelta.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bitdelta_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bd.LIB_PATH):
+        pytest.fail("libbitdelta.so is not built (run __graft_entry__.build())")
+    return bd.load_library()
+
+
+def test_header_declares_expected_api():
+    assert set(header_functions()) == set(bd.EXPORTED)
+
+
+def test_library_exports_every_header_symbol(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+
+
+def test_no_oracle_symbols_in_library():
+    # the product library must not contain (or link) the test oracle
+    data = open(bd.LIB_PATH, "rb").read()
+    assert b"oracle_" not in data
+
+
+def test_version_and_status_strings(lib):
+    assert lib.bitdelta_version() >= 100
+    for code in range(-7, 1):
+        s = bd.status_string(code)
+        assert s and s != "unknown status"
+    assert bd.status_string(-99) == "unknown status"
+
+
+# Fake, well-aligned device addresses: every call below must fail its host
+# checks (or be a no-op) before anything could dereference them.
+A = 0x10000000
+B = 0x20000000
+C = 0x30000000
+D = 0x40000000
+E = 0x50000000
+
+
+def mm(lib, x=A, M=4, K=64, w=B, N=8, p=C, alpha=D, tid=None, T=1, y=E, yd=bd.BF16,
+       path=bd.PATH_AUTO):
+    return lib.bitdelta_matmul_with_path(x, M, K, w, N, p, alpha, tid, T, y, yd, path, None)
+
+
+def test_matmul_shape_errors(lib):
+    assert mm(lib, K=48) == -2            # K % 32
+    assert mm(lib, M=-1) == -2
+    assert mm(lib, N=-3) == -2
+    assert mm(lib, K=-32) == -2
+    assert mm(lib, T=0) == -2
+    assert mm(lib, M=1 << 31) == -2
+
+
+def test_matmul_null_errors(lib):
+    assert mm(lib, x=None) == -1
+    assert mm(lib, w=None) == -1
+    assert mm(lib, p=None) == -1
+    assert mm(lib, alpha=None) == -1
+    assert mm(lib, y=None) == -1
+
+
+def test_matmul_alignment_errors(lib):
+    assert mm(lib, x=A + 2) == -3
+    assert mm(lib, w=B + 8) == -3
+    assert mm(lib, y=E + 4) == -3
+    assert mm(lib, p=C + 2) == -3
+    assert mm(lib, alpha=D + 1) == -3
+    assert mm(lib, tid=D + 0x1000 + 2) == -3
+
+
+def test_matmul_dtype_and_path_errors(lib):
+    assert mm(lib, yd=bd.I8) == -4
+    assert mm(lib, yd=7) == -4
+    assert mm(lib, path=9) == -5
+    assert mm(lib, tid=0x60000000, path=bd.PATH_PREFILL) == -5
+
+
+def test_matmul_alias_errors(lib):
+    # y overlapping x, w, packed, alpha or tenant ids
+    assert mm(lib, y=A) == -7
+    assert mm(lib, y=B + 256) == -7
+    assert mm(lib, y=C) == -7
+    assert mm(lib, y=D) == -7
+    assert mm(lib, tid=0x60000000, y=0x60000000) == -7
+
+
+def test_matmul_empty_is_noop(lib):
+    assert mm(lib, M=0) == 0
+    assert mm(lib, N=0) == 0
+    assert mm(lib, M=0, x=None, y=None) == 0
+
+
+def test_pack_unpack_errors(lib):
+    assert lib.bitdelta_pack(A, bd.F32, 4, 48, B, None) == -2
+    assert lib.bitdelta_pack(A, bd.F32, -1, 32, B, None) == -2
+    assert lib.bitdelta_pack(A, 5, 4, 32, B, None) == -4
+    assert lib.bitdelta_pack(None, bd.F32, 4, 32, B, None) == -1
+    assert lib.bitdelta_pack(A, bd.F32, 4, 32, None, None) == -1
+    assert lib.bitdelta_pack(A + 4, bd.F32, 4, 32, B, None) == -3   # f32 needs 16 B
+    assert lib.bitdelta_pack(A + 4, bd.BF16, 4, 32, B, None) == -3   # bf16 needs 8 B
+    assert lib.bitdelta_pack(A + 2, bd.I8, 4, 32, B, None) == -3    # i8 needs 4 B
+    assert lib.bitdelta_pack(A, bd.F32, 4, 32, B + 2, None) == -3
+    assert lib.bitdelta_pack(A, bd.F32, 4, 32, A + 64, None) == -7  # output inside input
+    assert lib.bitdelta_pack(A, bd.F32, 0, 32, B, None) == 0
+    assert lib.bitdelta_unpack(A, 4, 40, B, bd.F32, None) == -2
+    assert lib.bitdelta_unpack(A, 4, 32, B, 9, None) == -4
+    assert lib.bitdelta_unpack(None, 4, 32, B, bd.F32, None) == -1
+    assert lib.bitdelta_unpack(A, 4, 32, B + 8, bd.F32, None) == -3
+    assert lib.bitdelta_unpack(A, 4, 32, A, bd.F32, None) == -7
+    assert lib.bitdelta_unpack(A, 4, 0, B, bd.F32, None) == 0
+
+
+def test_path_selection(lib):
+    assert bd.matmul_path(1, 4096, 4096, 1, False) == bd.PATH_SKINNY
+    assert bd.matmul_path(64, 4096, 4096, 1, False) == bd.PATH_SKINNY
+    assert bd.matmul_path(65, 4096, 4096, 1, False) == bd.PATH_PREFILL
+    assert bd.matmul_path(4096, 4096, 4096, 1, False) == bd.PATH_PREFILL
+    assert bd.matmul_path(32, 11008, 4096, 16, True) == bd.PATH_SKINNY
+    assert bd.matmul_path(4096, 4096, 4096, 8, True) == bd.PATH_SKINNY

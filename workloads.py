@@ -147,7 +147,7 @@ def prefill(seed: int = 0) -> Problem:
 
 def llama_shared_inputs(seed: int = 0):
     """x for K=4096 and K=11008 (64 rows each) and the 64 tenant ids."""
-    rng = np.random.default_rng(seed)
+    rng = np.random.default_rng([seed, 1])
     x4096 = normal_bf16(rng, (LLAMA_ROWS, 4096), 1.0)
     x11008 = normal_bf16(rng, (LLAMA_ROWS, 11008), 1.0)
     tid = tenant_draw(rng, LLAMA_ROWS, LLAMA_TENANTS)
@@ -155,12 +155,17 @@ def llama_shared_inputs(seed: int = 0):
 
 
 def llama_matrix(layer: int, idx: int, shared=None, seed: int = 0) -> Problem:
-    """One matrix of the sweep, from sub-seed 1000*layer + idx (W, signs, alpha)."""
+    """One matrix of the sweep (W, signs, alpha), from its own seed sequence.
+
+    Seed sequences are tagged ([seed, 1] for the shared inputs, [seed, 2, layer,
+    idx] per matrix): numpy maps [s] and [s, 0] to the same stream, so untagged
+    sub-seeds could replay x as W.
+    """
     name, N, K = LLAMA_MATRICES[idx]
     if shared is None:
         shared = llama_shared_inputs(seed)
     x4096, x11008, tid = shared
-    rng = np.random.default_rng([seed, 1000 * layer + idx])
+    rng = np.random.default_rng([seed, 2, layer, idx])
     w = normal_bf16(rng, (N, K), 0.02)
     packed = uniform_words(rng, (LLAMA_TENANTS, N, K // 32))
     a = alphas(rng, LLAMA_TENANTS)
