@@ -1,0 +1,176 @@
+// Single-tenant decode GEMV/skinny kernel for M <= 16 token rows:
+//
+//   y[m][n] = sum_k x[m][k] W[n][k] + alpha * sum_k x[m][k] s[n][k]
+//
+// (the standard BitDelta GEMM of Section 4.4 at decode shapes).  Bound by HBM:
+// every byte of W and of the packed signs is read once.
+//
+// Work split: a 512-thread workgroup owns 16 output features; its 8 waves split
+// the contraction into contiguous runs of 32-wide k-blocks, processed in rounds
+// of D blocks.  Per round a wave
+//   * streams W straight into registers as MFMA B operands: one 16-byte load
+//     per lane per block (8 consecutive k of one feature), D loads in flight;
+//   * loads the packed signs of its 16 features x D blocks (D*4 bytes per row)
+//     with one coalesced 16-byte load per lane into a private LDS area;
+//   * loads its slice of x (up to 16 rows x D*64 bytes) with one coalesced
+//     1-KB load per row into the same area.
+// Scattered per-block loads of sign bytes and of x rows cost more request
+// slots than the W stream itself, so they go through LDS once per round and the
+// MFMA fragments are read back from there.  Signs become bf16 +1/-1 operands in
+// registers (decode_signs8, two values per two ops), and x*W^T and x*S^T are
+// accumulated apart in fp32 on v_mfma_f32_16x16x32_bf16; the epilogue forms
+// acc_base + alpha*acc_sign, so W + alpha*s is never rounded.
+//
+// Partial sums of the 8 waves are added in a fixed order through LDS: results
+// are bitwise deterministic.
+#include "device.h"
+#include "internal.h"
+
+namespace bitdelta {
+namespace {
+
+constexpr int kFeat = 16;        // output features per workgroup
+constexpr int kWaves = 8;
+constexpr int kRound = 16;       // k-blocks per wave per round (D)
+constexpr int kSignStride = 80;  // bytes per feature row of staged signs (64 + pad)
+
+template <int XR>
+struct DecodeLayout {
+    static constexpr int kXStride = kRound * 64 + 16;            // bytes per staged x row
+    static constexpr int kXBytes = XR * kXStride;
+    static constexpr int kWaveBytes = kXBytes + kFeat * kSignStride;
+    static constexpr int kTotal = kWaves * kWaveBytes;
+    static_assert(kTotal >= 2 * kWaves * 16 * kFeat * 4, "reduction area must fit");
+};
+
+__device__ __forceinline__ u32x4 lds_read16(const char* p) {
+    return *reinterpret_cast<const u32x4*>(p);
+}
+
+template <int XR>
+__global__ __launch_bounds__(kWaves * 64) void decode_kernel(
+    const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
+    const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
+    void* __restrict__ y, int y_dtype) {
+    using L = DecodeLayout<XR>;
+    __shared__ __attribute__((aligned(16))) char smem[L::kTotal];
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nl = lane & 15, g = lane >> 4;
+    const int n0 = blockIdx.x * kFeat;
+    const int KB = K >> 5, KW = K >> 5;
+
+    char* xs = smem + wv * L::kWaveBytes;        // staged x rows of this wave
+    char* ss = xs + L::kXBytes;                  // staged sign words of this wave
+
+    // W: this lane's feature (clamped; rows past N feed unstored outputs only)
+    const int n = min(n0 + nl, N - 1);
+    const uint16_t* wp = w + (size_t)n * K + 8 * g;
+    // signs: lane l stages row l/4, words 4*(l%4) .. +3 of the round
+    const int srow = lane >> 2, squad = lane & 3;
+    const uint32_t* sp = packed + (size_t)min(n0 + srow, N - 1) * KW;
+    // x: MFMA row nl reads staged row min(nl, XR-1); source rows clamped to M-1
+    const int xrow_lds = min(nl, XR - 1);
+
+    f32x4 accb = {0.f, 0.f, 0.f, 0.f}, accs = {0.f, 0.f, 0.f, 0.f};
+    const int per = (KB + kWaves - 1) / kWaves;
+    const int kb0 = min(KB, wv * per);
+    const int kb1 = min(KB, kb0 + per);
+    const bool aligned_signs = (KW & 3) == 0;
+
+    for (int base = kb0; base < kb1; base += kRound) {
+        const int c = min(kRound, kb1 - base);   // blocks in this round (uniform)
+
+        // ---- issue: signs, x slice, then the W stream (oldest first) ----
+        uint32_t sw[4];
+        if (aligned_signs && c == kRound && (base & 3) == 0) {
+            const u32x4 v = *reinterpret_cast<const u32x4*>(sp + base + 4 * squad);
+            sw[0] = v[0]; sw[1] = v[1]; sw[2] = v[2]; sw[3] = v[3];
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sw[i] = sp[base + min(4 * squad + i, c - 1)];
+        }
+        u32x4 xv[XR];
+        const int xchunk = min(lane, 4 * c - 1);   // 16-byte chunk of the row slice
+#pragma unroll
+        for (int r = 0; r < XR; ++r)
+            xv[r] = load16(x + (size_t)min(r, M - 1) * K + (size_t)base * 32 + 8 * xchunk);
+        __builtin_amdgcn_sched_barrier(0);
+        u32x4 wf[kRound];
+#pragma unroll
+        for (int j = 0; j < kRound; ++j) {
+            wf[j] = load16(wp + (size_t)(base + min(j, c - 1)) * 32);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+
+        // ---- stage signs and x in this wave's LDS area ----
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            *reinterpret_cast<uint32_t*>(ss + srow * kSignStride + 16 * squad + 4 * i) = sw[i];
+#pragma unroll
+        for (int r = 0; r < XR; ++r)
+            *reinterpret_cast<u32x4*>(xs + r * L::kXStride + 16 * lane) = xv[r];
+
+        // ---- consume, oldest block first ----
+        auto consume = [&](int j) {
+            const u32x4 xa = lds_read16(xs + xrow_lds * L::kXStride + j * 64 + 16 * g);
+            const uint32_t sb = *reinterpret_cast<const uint8_t*>(ss + nl * kSignStride + 4 * j + g);
+            accb = mfma16(xa, wf[j], accb);
+            accs = mfma16(xa, decode_signs8(sb), accs);
+        };
+        if (c == kRound) {
+#pragma unroll
+            for (int j = 0; j < kRound; ++j) consume(j);
+        } else {
+#pragma unroll
+            for (int j = 0; j < kRound; ++j)
+                if (j < c) consume(j);
+        }
+    }
+
+    // ---- combine the waves' partial sums (fixed order) ----
+    __syncthreads();
+    float* red_b = reinterpret_cast<float*>(smem);                 // [wave][16 rows][16 feat]
+    float* red_s = red_b + kWaves * 16 * kFeat;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        red_b[(wv * 16 + 4 * g + r) * kFeat + nl] = accb[r];
+        red_s[(wv * 16 + 4 * g + r) * kFeat + nl] = accs[r];
+    }
+    __syncthreads();
+    if (threadIdx.x < 16 * kFeat) {
+        const int m = threadIdx.x / kFeat, f = threadIdx.x % kFeat;
+        const int nn = n0 + f;
+        if (m < M && nn < N) {
+            float b = 0.f, s = 0.f;
+#pragma unroll
+            for (int v = 0; v < kWaves; ++v) {
+                b += red_b[(v * 16 + m) * kFeat + f];
+                s += red_s[(v * 16 + m) * kFeat + f];
+            }
+            const float out = __builtin_fmaf(alpha[0], s, b);
+            if (y_dtype == kF32)
+                reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
+            else
+                reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                         const uint32_t* packed, const float* alpha, void* y, int y_dtype,
+                         hipStream_t stream) {
+    const int grid = (N + kFeat - 1) / kFeat;
+    if (M == 1)
+        decode_kernel<1><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    else if (M <= 4)
+        decode_kernel<4><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    else
+        decode_kernel<16><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    return hipGetLastError();
+}
+
+}  // namespace bitdelta

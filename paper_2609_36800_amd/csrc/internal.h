@@ -19,6 +19,11 @@ hipError_t launch_pack(const void* signs, int dtype, int64_t elems, uint32_t* pa
 hipError_t launch_unpack(const uint32_t* packed, int64_t elems, void* signs, int dtype,
                          hipStream_t stream);
 
+// Single-tenant decode matmul for at most 16 rows (signs and x staged via LDS).
+hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                         const uint32_t* packed, const float* alpha, void* y, int y_dtype,
+                         hipStream_t stream);
+
 // Decode-shaped matmul for at most 64 rows (any number of tenants).
 hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha,

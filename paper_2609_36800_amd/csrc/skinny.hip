@@ -56,29 +56,31 @@ __device__ __forceinline__ void wave_range(int KB, int wv, int nw, int& kb0, int
     kb1 = min(KB, kb0 + per);
 }
 
-template <int MB, int NW, int U>
+// Single tenant.  Each wave streams a contiguous run of k-blocks through a
+// ring of D register stages: the loads of block i+D are issued right after
+// block i is consumed, so up to D blocks per lane stay in flight.  Loads are
+// never predicated: rows beyond M or N are clamped onto the last valid row
+// (they only feed output rows/columns that are not stored), which keeps the
+// loads free of branches and lets the compiler wait on the oldest stage only.
+template <int MB, int NW, int D>
 __global__ __launch_bounds__(NW * 64) void skinny_single_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
     void* __restrict__ y, int y_dtype) {
     __shared__ SkinnyLds<MB, NW> sh;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int nl = lane & 15, g = lane >> 4;
     const int n0 = blockIdx.x * kFeat;
-    const int n = n0 + nl;
-    const bool nvalid = n < N;
     const int KB = K >> 5, KW = K >> 5;
 
-    const uint16_t* wrow = w + (size_t)(nvalid ? n : 0) * K + 8 * g;
-    const uint32_t* srow = packed + (size_t)(nvalid ? n : 0) * KW;
-    const uint16_t* xrow[MB];
-    bool xvalid[MB];
+    const int n = min(n0 + nl, N - 1);
+    const uint16_t* wp = w + (size_t)n * K + 8 * g;
+    // byte g of each sign word holds the signs of this lane's eight k
+    const uint8_t* sp = reinterpret_cast<const uint8_t*>(packed + (size_t)n * KW) + g;
+    const uint16_t* xp[MB];
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-        const int m = mb * 16 + nl;
-        xvalid[mb] = m < M;
-        xrow[mb] = x + (size_t)(xvalid[mb] ? m : 0) * K + 8 * g;
-    }
+    for (int mb = 0; mb < MB; ++mb) xp[mb] = x + (size_t)min(mb * 16 + nl, M - 1) * K + 8 * g;
 
     f32x4 accb[MB], accs[MB];
 #pragma unroll
@@ -89,34 +91,45 @@ __global__ __launch_bounds__(NW * 64) void skinny_single_kernel(
 
     int kb0, kb1;
     wave_range(KB, wv, NW, kb0, kb1);
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-
-    auto run = [&](int kb, auto unroll_tag) {
-        constexpr int UU = decltype(unroll_tag)::value;
-        u32x4 wf[UU];
-        uint32_t sw[UU];
-        u32x4 xf[UU][MB];
+    const int cnt = kb1 - kb0;
+    if (cnt > 0) {
+        u32x4 wf[D];
+        uint32_t sb[D];
+        u32x4 xf[D][MB];
+        auto issue = [&](int slot, int kb) {
+            wf[slot] = load16(wp + kb * 32);
+            sb[slot] = sp[kb * 4];
 #pragma unroll
-        for (int u = 0; u < UU; ++u) {
-            const int k = (kb + u) * 32;
-            wf[u] = nvalid ? load16(wrow + k) : zero;
-            sw[u] = nvalid ? srow[kb + u] : 0u;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) xf[u][mb] = xvalid[mb] ? load16(xrow[mb] + k) : zero;
-        }
-#pragma unroll
-        for (int u = 0; u < UU; ++u) {
-            const u32x4 sf = decode_signs8(sign_byte(sw[u], g));
+            for (int mb = 0; mb < MB; ++mb) xf[slot][mb] = load16(xp[mb] + kb * 32);
+            // keep stages in issue order: the oldest stage must complete first
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        auto consume = [&](int slot) {
+            const u32x4 sf = decode_signs8(sb[slot]);
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) {
-                accb[mb] = mfma16(xf[u][mb], wf[u], accb[mb]);
-                accs[mb] = mfma16(xf[u][mb], sf, accs[mb]);
+                accb[mb] = mfma16(xf[slot][mb], wf[slot], accb[mb]);
+                accs[mb] = mfma16(xf[slot][mb], sf, accs[mb]);
+            }
+        };
+        // Rounds of D blocks: all D loads of a round are issued back to back
+        // (in order), then consumed oldest first, each block waiting only for
+        // its own stage.  A wave's whole share is one round when K <= 32*D*NW.
+        for (int base = 0; base < cnt; base += D) {
+            const int c = min(D, cnt - base);
+#pragma unroll
+            for (int j = 0; j < D; ++j) issue(j, kb0 + base + min(j, c - 1));
+            if (c == D) {
+                // full round: no guards, so no load can be sunk past its successors
+#pragma unroll
+                for (int j = 0; j < D; ++j) consume(j);
+            } else {
+#pragma unroll
+                for (int j = 0; j < D; ++j)
+                    if (j < c) consume(j);
             }
         }
-    };
-    int kb = kb0;
-    for (; kb + U <= kb1; kb += U) run(kb, std::integral_constant<int, U>{});
-    for (; kb < kb1; ++kb) run(kb, std::integral_constant<int, 1>{});
+    }
 
     // lane holds D(row 4g + r, feature nl) of each 16-row block
 #pragma unroll
@@ -153,7 +166,8 @@ __global__ __launch_bounds__(NW * 64) void skinny_multi_kernel(
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
     const int32_t* __restrict__ tenant_ids, int T, void* __restrict__ y, int y_dtype) {
     __shared__ SkinnyLds<MB, NW> sh;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int nl = lane & 15, g = lane >> 4;
     const int n0 = blockIdx.x * kFeat;
     const int n = n0 + nl;
@@ -314,8 +328,8 @@ hipError_t launch_single_mb(const uint16_t* x, int M, int K, const uint16_t* w, 
                             const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                             hipStream_t stream) {
     const int grid = (N + kFeat - 1) / kFeat;
-    constexpr int U = MB <= 2 ? 8 : 4;
-    skinny_single_kernel<MB, kWaves, U><<<grid, kWaves * 64, 0, stream>>>(
+    constexpr int D = MB == 1 ? 16 : (MB == 2 ? 12 : 8);
+    skinny_single_kernel<MB, kWaves, D><<<grid, kWaves * 64, 0, stream>>>(
         x, M, K, w, N, packed, alpha, y, y_dtype);
     return hipGetLastError();
 }
@@ -338,6 +352,7 @@ hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int
                          hipStream_t stream) {
     const int mb = (M + 15) / 16;
     if (tenant_ids == nullptr) {
+        if (M <= 16) return launch_decode(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
         switch (mb) {
             case 1: return launch_single_mb<1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
             case 2: return launch_single_mb<2>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
