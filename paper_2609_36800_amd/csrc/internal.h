@@ -24,6 +24,13 @@ hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                          hipStream_t stream);
 
+// Batched (multi-tenant) matmul for at most 64 rows, operands staged in LDS by
+// global->LDS copies; needs K a positive multiple of 128 (multi_supported).
+bool multi_supported(int K);
+hipError_t launch_multi(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                        const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
+                        int T, void* y, int y_dtype, hipStream_t stream);
+
 // Decode-shaped matmul for at most 64 rows (any number of tenants).
 hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha,

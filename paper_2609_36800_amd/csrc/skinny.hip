@@ -360,6 +360,8 @@ hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int
             default: return launch_single_mb<4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
         }
     }
+    if (multi_supported(K))
+        return launch_multi(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
     switch (mb) {
         case 1: return launch_multi_mb<1>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
         case 2: return launch_multi_mb<2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
