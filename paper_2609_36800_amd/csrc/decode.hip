@@ -25,6 +25,7 @@
 // are bitwise deterministic.
 #include "device.h"
 #include "internal.h"
+#include "ldscopy.h"
 
 namespace bitdelta {
 namespace {
@@ -158,11 +159,188 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// Streaming variant (K a multiple of 128): W and x reach LDS by global->LDS
+// copies in 256-k tiles, NB-1 tiles ahead of the one being computed, and the
+// workgroup's sign words for the whole K are staged once up front.  Each copy
+// instruction moves whole 512-byte row segments, so every request is a full
+// cache line (the register path above issues 64-byte half lines), and the
+// streaming does not depend on how many waves are resident.  In tile t wave w
+// computes k-block 8t + w from LDS; one vmcnt wait plus one barrier per tile.
+// ---------------------------------------------------------------------------
+constexpr int kTileBlocks = 8;                  // k-blocks per tile (one per wave)
+constexpr int kTileRow = kTileBlocks * 64;      // bytes of one row segment of a tile
+
+// XUP: x (XR rows x K <= 4096) is staged once up front instead of per tile.
+template <int XR, bool XUP>
+struct StreamCfg {
+    static constexpr int kWBytes = kFeat * kTileRow;          // W: 16 rows x 512 B
+    static constexpr int kXBytes = XUP ? 0 : XR * kTileRow;   // x: XR rows x 512 B per tile
+    static constexpr int kTileBytes = kWBytes + kXBytes;
+    static constexpr int kNB = 6;                             // ring depth (tiles)
+    static constexpr int kRing = kNB * kTileBytes;
+    static constexpr int kOpsPerTile = XUP ? 1 : 2;           // copies per wave per tile
+    static constexpr int kXLanes = XR * 4;                    // lanes of a wave copying x
+    static constexpr int kXRowUp = 4096 * 2 + 64;             // up-front x row stride (padded)
+    static constexpr int kXUpBytes = XUP ? XR * kXRowUp : 0;
+};
+
+__device__ __forceinline__ int tswz(int row, int chunk) { return chunk ^ (row & 15); }
+
+// SB: bytes reserved for the staged signs (16 features x K/8 bytes).
+template <int XR, int SB, bool XUP>
+__global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
+    const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
+    const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
+    void* __restrict__ y, int y_dtype) {
+    using C = StreamCfg<XR, XUP>;
+    constexpr int NB = C::kNB;
+    constexpr int D = NB - 1;
+    static_assert(C::kRing >= 2 * kWaves * 16 * kFeat * 4, "reduction area must fit");
+    __shared__ __attribute__((aligned(16))) char lds[C::kRing + SB + C::kXUpBytes];
+    char* ring = lds;
+    char* sg = lds + C::kRing;      // signs: [chunk of 4 words][feature][16 B]
+    char* xu = sg + SB;             // up-front x rows (XUP)
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nl = lane & 15, g = lane >> 4;
+    const int n0 = blockIdx.x * kFeat;
+    const int KB = K >> 5, KW = K >> 5;
+    const int KT = (KB + kTileBlocks - 1) / kTileBlocks;
+
+    // ---- stage all sign words of the 16 features (same count on every wave) ----
+    {
+        const int nq = (KW + 15) >> 4;                        // copies of 4 chunks x 16 features
+        const int per_wave = (nq + kWaves - 1) / kWaves;
+        const uint32_t* srow = packed + (size_t)min(n0 + (lane & 15), N - 1) * KW;
+        for (int i = 0; i < per_wave; ++i) {
+            const int q = min(wv + i * kWaves, nq - 1);       // surplus copies repeat the last one
+            const int chunk = min(4 * q + (lane >> 4), KW / 4 - 1);
+            copy16_to_lds(srow + 4 * chunk, sg + q * 1024);
+        }
+    }
+
+    // ---- up-front x (XUP): XR rows x K, 1 KB per copy, same count on every wave ----
+    if constexpr (XUP) {
+        // a row of 2K bytes takes ceil(2K / 1 KB) copies; lanes past the row's end
+        // re-read its last 16 bytes into the unused tail of the padded row stride
+        const int per_row = (K + 511) >> 9;
+        const int nx = XR * per_row;
+        const int per_wave = (nx + kWaves - 1) / kWaves;
+        for (int i = 0; i < per_wave; ++i) {
+            const int q = min(wv + i * kWaves, nx - 1);
+            const int r = q / per_row, part = q - r * per_row;
+            const int e = min(part * 512 + 8 * lane, K - 8);
+            copy16_to_lds(x + (size_t)min(r, M - 1) * K + e, xu + r * C::kXRowUp + part * 1024);
+        }
+    }
+
+    // ---- ring of W and x tiles ----
+    const int wf = 2 * wv + (lane >> 5), wslot = lane & 31;
+    const int wchunk = tswz(wf, wslot);
+    const uint16_t* wsrc = w + (size_t)min(n0 + wf, N - 1) * K;
+    const int xidx = wv * C::kXLanes + lane;                  // chunk index inside the x tile
+    const int xr = xidx >> 5, xchunk = tswz(xr, xidx & 31);
+    const uint16_t* xsrc = x + (size_t)min(xr, M - 1) * K;
+    auto issue_tile = [&](int tt) {
+        const int tc = min(tt, KT - 1);                       // tail tiles repeat the last one
+        char* buf = ring + (tt % NB) * C::kTileBytes;
+        const int kbw = min(tc * kTileBlocks + (wchunk >> 2), KB - 1);
+        copy16_to_lds(wsrc + (size_t)kbw * 32 + 8 * (wchunk & 3), buf + wv * 1024);
+        if (!XUP && lane < C::kXLanes) {
+            const int kbx = min(tc * kTileBlocks + (xchunk >> 2), KB - 1);
+            copy16_to_lds(xsrc + (size_t)kbx * 32 + 8 * (xchunk & 3),
+                          buf + C::kWBytes + wv * (C::kXLanes * 16));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    const int c = 4 * wv + g;                                 // this lane's chunk of a tile row
+    const int woff = nl * kTileRow + 16 * tswz(nl, c);
+    const int xrow = min(nl, XR - 1);
+    const int xoff = C::kWBytes + xrow * kTileRow + 16 * tswz(xrow, c);
+    f32x4 accb = {0.f, 0.f, 0.f, 0.f}, accs = {0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int i = 0; i < D; ++i) issue_tile(i);
+    for (int t = 0; t < KT; ++t) {
+        wait_vm_lgkm0<(D - 1) * C::kOpsPerTile>();
+        raw_barrier();
+        issue_tile(t + D);              // into the buffer of tile t-1, free after the barrier
+        const int kb = t * kTileBlocks + wv;
+        if (kb < KB) {
+            const char* buf = ring + (t % NB) * C::kTileBytes;
+            const u32x4 bw = *reinterpret_cast<const u32x4*>(buf + woff);
+            const u32x4 xa = XUP ? *reinterpret_cast<const u32x4*>(xu + xrow * C::kXRowUp + kb * 64 + 16 * g)
+                                 : *reinterpret_cast<const u32x4*>(buf + xoff);
+            const uint32_t sb = *reinterpret_cast<const uint8_t*>(
+                sg + (kb >> 2) * 256 + nl * 16 + 4 * (kb & 3) + g);
+            accb = mfma16(xa, bw, accb);
+            accs = mfma16(xa, decode_signs8(sb), accs);
+        }
+    }
+    wait_vm_lgkm0<0>();
+    __syncthreads();
+
+    // ---- combine the waves' partial sums (fixed order) ----
+    float* red_b = reinterpret_cast<float*>(lds);             // [wave][16 rows][16 feat]
+    float* red_s = red_b + kWaves * 16 * kFeat;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        red_b[(wv * 16 + 4 * g + r) * kFeat + nl] = accb[r];
+        red_s[(wv * 16 + 4 * g + r) * kFeat + nl] = accs[r];
+    }
+    __syncthreads();
+    if (threadIdx.x < 16 * kFeat) {
+        const int m = threadIdx.x / kFeat, f = threadIdx.x % kFeat;
+        const int nn = n0 + f;
+        if (m < M && nn < N) {
+            float b = 0.f, s = 0.f;
+#pragma unroll
+            for (int v = 0; v < kWaves; ++v) {
+                b += red_b[(v * 16 + m) * kFeat + f];
+                s += red_s[(v * 16 + m) * kFeat + f];
+            }
+            const float out = __builtin_fmaf(alpha[0], s, b);
+            if (y_dtype == kF32)
+                reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
+            else
+                reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+        }
+    }
+}
+
+template <int XR>
+hipError_t launch_stream(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                         const uint32_t* packed, const float* alpha, void* y, int y_dtype,
+                         hipStream_t stream) {
+    const int grid = (N + kFeat - 1) / kFeat;
+    if constexpr (XR <= 4) {
+        if (K <= 4096) {
+            stream_decode_kernel<XR, 8192, true><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+            return hipGetLastError();
+        }
+    }
+    if (K <= 4096)
+        stream_decode_kernel<XR, 8192, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    else
+        stream_decode_kernel<XR, 32768, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                          hipStream_t stream) {
+    if (K >= 128 && (K & 127) == 0 && K <= 16384) {
+        // signs of 16 features x K fit the staging area; rows of W split into whole chunks
+        if (M == 1) return launch_stream<1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+        if (M <= 4) return launch_stream<4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+        return launch_stream<16>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+    }
     const int grid = (N + kFeat - 1) / kFeat;
     if (M == 1)
         decode_kernel<1><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);

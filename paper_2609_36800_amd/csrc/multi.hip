@@ -33,11 +33,10 @@
 // deterministic.
 #include "device.h"
 #include "internal.h"
+#include "ldscopy.h"
 
 namespace bitdelta {
 namespace {
-
-typedef __attribute__((address_space(3))) void lvoid;
 
 constexpr int kFeat = 16;
 constexpr int kWaves = 8;
@@ -59,29 +58,6 @@ struct MultiCfg {
     static constexpr int kRedBytes = 2 * kWaves * kRowsMax * kFeat * 4;
     static constexpr int kLdsBytes = kRingBytes > kRedBytes ? kRingBytes : kRedBytes;
 };
-
-// s_waitcnt with vmcnt = n, lgkmcnt = 0, expcnt untouched (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4));
-}
-
-__device__ __forceinline__ void raw_barrier() {
-    // LDS copies are ordered by the explicit vmcnt wait above, LDS writes by
-    // lgkmcnt(0); the clobber keeps the compiler from moving memory ops across.
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
-// One global -> LDS copy of 16 bytes per lane: lane l's bytes land at
-// lds_base + 16*l.  Issued as inline asm so that the compiler does not model
-// the LDS write and therefore does not drain every copy in flight before each
-// LDS read; visibility is established explicitly by wait_vm_lgkm0 + barrier.
-__device__ __forceinline__ void copy16_to_lds(const void* src, void* lds_base) {
-    const uint32_t lds_off = (uint32_t)(uintptr_t)(lvoid*)lds_base;
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(lds_off), "v"(src) : "memory", "m0");
-}
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
 
