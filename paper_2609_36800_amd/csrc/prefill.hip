@@ -8,21 +8,44 @@
 // to the matrix unit (Appendix A.2).  The price is one bf16 rounding of the
 // effective weight (alpha is tiny next to |W|, so it shifts W by a few ulps).
 //
-// Tiling for gfx950: a 256-thread workgroup (4 waves, 2x2) owns a 256x256
-// output tile; each wave owns 128x128 = 4x4 v_mfma_f32_32x32x16_bf16 tiles
-// (256 fp32 accumulators per lane).  K advances in 64-wide tiles staged in LDS
-// (double-buffered, 64 KB per stage).  Each thread moves eight 16-byte chunks
-// of x and eight of W per tile with coalesced 128-bit loads plus the matching
-// sign bytes; W chunks are fused with alpha*s in registers on their way to LDS,
-// so every element of W_eff is decoded once per workgroup, not once per wave.
-// LDS rows are 128 bytes; chunk c of row r is stored at slot c ^ (r & 7) so
-// that the fragment reads of eight consecutive rows hit distinct banks.
+// Two kernels share that contraction and the output tiling:
+//
+// prefill_stream_kernel (K a multiple of 64; the common case).  A 256-thread
+// workgroup (4 waves, 2x2) owns a 256x256 output tile, each wave 128x128 =
+// 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane).  Per
+// 64-wide k-tile:
+//   * the x tile is copied global -> LDS by the DMA path (no VGPR staging),
+//     one tile ahead, into one of two LDS buffers;
+//   * the raw W tile and its sign words are loaded into registers two tiles
+//     ahead (two register sets), and the effective weights of the next tile
+//     are formed and written to the other of two LDS buffers while the
+//     matrix cores work on the current one: the 64 MFMAs of a k-tile are
+//     issued one per scheduling slot, and each slot carries a share of the
+//     decode (one bf16 pair), the LDS writes and the next loads;
+//   * one barrier per k-tile publishes both buffers.
+// The two LDS buffers of each operand are separate objects so the compiler
+// can tell a copy into one from a read of the other and count the copies
+// exactly when it places its waits.
+// Every W element is decoded once per workgroup; with alpha's sign moved onto
+// W (s*W + alpha, rounded, then the sign restored -- round-to-nearest-even is
+// symmetric) all eight weights of a chunk add the same alpha.
+//
+// prefill_general_kernel (any K that is a multiple of 32): the same tiling
+// with both operands staged through registers and zero-filled past K.
+//
+// LDS rows are 128 bytes (64 bf16).  Chunk c of row r is stored at slot
+// c ^ f(r), f(r) = (r & 7) ^ ((r >> 3) & 1): the 16-byte fragment reads of 16
+// consecutive rows then fall in distinct bank groups whether LDS serves 8 or
+// 16 lanes of a 128-bit read per cycle.
 //
 // Workgroups are renumbered so that the 32 resident on one XCD (the hardware
 // deals workgroups round-robin over the 8 XCDs) cover a 4 x 8 block of tiles
 // and share their x and W panels in that XCD's L2.
+#include <type_traits>
+
 #include "device.h"
 #include "internal.h"
+#include "ldscopy.h"
 
 namespace bitdelta {
 namespace {
@@ -38,10 +61,10 @@ struct PrefillLds {
 };
 
 __device__ __forceinline__ int lds_off(int row, int chunk) {
-    return row * BK + ((chunk ^ (row & 7)) << 3);
+    return row * BK + ((chunk ^ (row & 7) ^ ((row >> 3) & 1)) << 3);
 }
 
-__global__ __launch_bounds__(kThreads, 1) void prefill_kernel(
+__global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
     void* __restrict__ y, int y_dtype, int tiles_m, int tiles_n) {
@@ -167,6 +190,263 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_kernel(
         }
 }
 
+// ------------------------------------------------------------ streaming kernel
+
+// Output-tile assignment shared by both kernels (XCD-aware, groups of kGroupM
+// tile rows).
+__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tile_m, int& tile_n) {
+    const int nwg = tiles_m * tiles_n;
+    int bid = blockIdx.x;
+    if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
+    const int group = bid / (kGroupM * tiles_n);
+    const int first_m = group * kGroupM;
+    const int gm = min(tiles_m - first_m, kGroupM);
+    const int local = bid - group * kGroupM * tiles_n;
+    tile_m = first_m + local % gm;
+    tile_n = local / gm;
+}
+
+template <int P, class T>
+__device__ __forceinline__ T& pick(T& a, T& b) {
+    if constexpr (P == 0) return a; else return b;
+}
+
+// Hides a value from the optimiser so that a shift-and-mask sequence built on
+// it is emitted as written.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
+typedef __attribute__((ext_vector_type(2))) float f32x2v;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2v;
+
+// One bf16 pair of effective weights, in two halves of four VALU operations
+// so that the work can be spread over two MFMA issue slots.  `s` carries the
+// chunk's eight sign bits twice (bit i and bit i+15); shifting by 15-2p
+// brings the bits of pair p to positions 15 and 31.  A clear bit (sign -1)
+// flips the sign of that weight, alpha is added in fp32, the sum is rounded to
+// bf16 (v_cvt_pk_bf16_f32, round to nearest even) and the flip is undone.
+struct PairWork {
+    uint32_t xm;
+    float lo, hi;
+};
+
+__device__ __forceinline__ PairWork fuse_pair_a(uint32_t w, uint32_t s, int p) {
+    PairWork r;
+    r.xm = ~(s << (15 - 2 * p));
+    const uint32_t v = w ^ (r.xm & kSignBits);
+    r.lo = __builtin_bit_cast(float, v << 16);
+    r.hi = __builtin_bit_cast(float, v & 0xFFFF0000u);
+    return r;
+}
+
+__device__ __forceinline__ uint32_t fuse_pair_b(const PairWork& q, float alpha) {
+    const f32x2v f = {q.lo + alpha, q.hi + alpha};
+    const uint32_t r = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
+    return r ^ (q.xm & kSignBits);
+}
+
+__device__ __forceinline__ uint32_t fuse_pair(uint32_t w, uint32_t s, int p, float alpha) {
+    return fuse_pair_b(fuse_pair_a(w, s, p), alpha);
+}
+
+__global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
+    const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
+    const uint32_t* __restrict__ packed, const float* __restrict__ alpha_p,
+    void* __restrict__ y, int y_dtype, int tiles_m, int tiles_n) {
+    // Two buffers per operand, each [256 rows][64 k] bf16 = 32 KB.
+    __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
+    __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
+    __shared__ __attribute__((aligned(1024))) uint16_t sB0[BN * BK];
+    __shared__ __attribute__((aligned(1024))) uint16_t sB1[BN * BK];
+
+    int tile_m, tile_n;
+    tile_of(tiles_m, tiles_n, tile_m, tile_n);
+    const int m0 = tile_m * BM, n0 = tile_n * BN;
+
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wv >> 1, wn = wv & 1;
+    const int KT = K / BK;
+    const int KW = K >> 5;
+    const float alpha = alpha_p[0];
+
+    // ---- staging assignment: per instruction i a wave moves rows
+    //      32i + 8wv + (lane >> 3), lane l landing at LDS slot l & 7 ----
+    const int fst = (lane >> 3) ^ (wv & 1);          // f(row) of the staged rows
+    const int ch = (lane & 7) ^ fst;                 // global 16-byte chunk moved
+    uint32_t xoff[8], woff[8], soff[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int r = 32 * i + 8 * wv + (lane >> 3);
+        const uint32_t xr = (uint32_t)min(m0 + r, M - 1);
+        const uint32_t wr = (uint32_t)min(n0 + r, N - 1);
+        xoff[i] = (xr * (uint32_t)K + 8u * ch) * 2u;
+        woff[i] = (wr * (uint32_t)K + 8u * ch) * 2u;
+        soff[i] = (wr * (uint32_t)KW + (uint32_t)(ch >> 2)) * 4u;
+    }
+    const int sbit = (ch & 3) * 8;
+    const int st_lane = 8 * wv * BK + 8 * lane;      // bf16 offset of the lane's slot, row block 0
+
+    // ---- fragment reads: row (lane & 31) of a 32-row block, chunk 2kk + (lane >> 5) ----
+    const int frd = (lane & 7) ^ ((lane >> 3) & 1);
+    int rdo[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) rdo[kk] = (lane & 31) * BK + 8 * ((2 * kk + (lane >> 5)) ^ frd);
+    const int a_row0 = wm * 128 * BK, b_row0 = wn * 128 * BK;
+
+    const char* xg = reinterpret_cast<const char*>(x);
+    const char* wg = reinterpret_cast<const char*>(w);
+    const char* sg = reinterpret_cast<const char*>(packed);
+
+    auto load_w = [&](u32x4& dst, int i, int kt) {
+        dst = *reinterpret_cast<const u32x4*>(wg + (size_t)kt * (BK * 2) + woff[i]);
+    };
+    auto load_s = [&](uint32_t& dst, int i, int kt) {
+        dst = *reinterpret_cast<const uint32_t*>(sg + (size_t)kt * 8 + soff[i]);
+    };
+    auto copy_x = [&](uint16_t* dst, int kt) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            __builtin_amdgcn_global_load_lds(xg + (size_t)kt * (BK * 2) + xoff[i],
+                                             dst + (32 * i + 8 * wv) * BK, 16, 0, 0);
+    };
+    auto sign_word = [&](uint32_t d) {
+        const uint32_t byte = (d >> sbit) & 0xFFu;
+        return opaque(byte | (byte << 15));
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // Register sets of raw W / sign words: set (t & 1) holds tile t + 2 while
+    // tile t is multiplied... precisely, iteration t decodes set (t + 1) & 1
+    // (tile t + 1) and refills it with tile t + 3.
+    u32x4 w0[8], w1[8];
+    uint32_t s0[8], s1[8];
+
+    // ---- prologue: tile 0 decoded into sB0, x tile 0 copied, tiles 1, 2 loaded ----
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, 0); load_s(s0[i], i, 0); }
+    copy_x(sA0, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { load_w(w1[i], i, min(1, KT - 1)); load_s(s1[i], i, min(1, KT - 1)); }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint32_t s = sign_word(s0[i]);
+        u32x4 o;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w0[i][p], s, p, alpha);
+        *reinterpret_cast<u32x4*>(sB0 + i * 32 * BK + st_lane) = o;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, min(2, KT - 1)); load_s(s0[i], i, min(2, KT - 1)); }
+
+    auto step = [&](auto par, int t) {
+        constexpr int P = decltype(par)::value;
+        uint16_t* const Ac = P ? sA1 : sA0;
+        uint16_t* const An = P ? sA0 : sA1;
+        uint16_t* const Bc = P ? sB1 : sB0;
+        uint16_t* const Bn = P ? sB0 : sB1;
+        u32x4(&ws)[8] = pick<P ^ 1>(w0, w1);
+        uint32_t(&ss)[8] = pick<P ^ 1>(s0, s1);
+
+        // x tile t and the raw W of tile t + 1 were issued before the last 16
+        // loads (the W/sign loads of the previous iteration); this wave's LDS
+        // writes of tile t are done.  The barrier publishes both to all waves.
+        asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+
+        u32x4 fa[4], fb[4], na[4], nb[4];
+        // read order a0 b0 b1 b2 b3 a1 a2 a3 follows the MFMA order below, so
+        // the first MFMA waits for two reads only
+        fa[0] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + rdo[0]);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            fb[j] = *reinterpret_cast<const u32x4*>(Bc + b_row0 + j * 32 * BK + rdo[0]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int i = 1; i < 4; ++i) {
+            fa[i] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + i * 32 * BK + rdo[0]);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        copy_x(An, min(t + 1, KT - 1));
+        const int kw = min(t + 3, KT - 1);
+        uint32_t sw = sign_word(ss[0]);
+        __builtin_amdgcn_sched_barrier(0);
+
+        // Slot g = 16kk + m issues MFMA (m / 4, m % 4) of k-step kk and half a
+        // pair of chunk c = g / 8: u = g % 8 even -> first half of pair u / 2,
+        // odd -> second half.  Chunk c is written to LDS in the slot after its
+        // last half; its registers are refilled with tile t + 3 once consumed.
+        PairWork pw;
+        u32x4 o, o_prev;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+            for (int m = 0; m < 16; ++m) {
+                const int i = m >> 2, j = m & 3;
+                acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
+                if (kk < 3 && m < 8) {
+                    if (m == 0) na[0] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + rdo[kk + 1]);
+                    else if (m < 5) nb[m - 1] = *reinterpret_cast<const u32x4*>(Bc + b_row0 + (m - 1) * 32 * BK + rdo[kk + 1]);
+                    else na[m - 4] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + (m - 4) * 32 * BK + rdo[kk + 1]);
+                }
+                const int g = kk * 16 + m, c = g >> 3, u = g & 7;
+                if (u == 0 && c > 0) *reinterpret_cast<u32x4*>(Bn + (c - 1) * 32 * BK + st_lane) = o_prev;
+                if ((u & 1) == 0) pw = fuse_pair_a(ws[c][u >> 1], sw, u >> 1);
+                else o[u >> 1] = fuse_pair_b(pw, alpha);
+                if (u == 6) load_s(ss[c], c, kw);
+                if (u == 7) {
+                    load_w(ws[c], c, kw);
+                    if (c < 7) sw = sign_word(ss[c + 1]);
+                    o_prev = o;
+                }
+                if (g == 63) *reinterpret_cast<u32x4*>(Bn + 7 * 32 * BK + st_lane) = o;
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if (kk < 3) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) { fa[r] = na[r]; fb[r] = nb[r]; }
+            }
+        }
+    };
+
+    int t = 0;
+    for (; t + 1 < KT; t += 2) {
+        step(std::integral_constant<int, 0>{}, t);
+        step(std::integral_constant<int, 1>{}, t + 1);
+    }
+    if (t < KT) step(std::integral_constant<int, 0>{}, t);
+    // copies issued for tiles past the end still target LDS: drain them
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+    // ---- epilogue: lane holds column (lane & 31) of each 32x32 tile ----
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int col = n0 + wn * 128 + j * 32 + (lane & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (row < M && col < N) {
+                    if (y_dtype == kF32)
+                        reinterpret_cast<float*>(y)[(size_t)row * N + col] = acc[i][j][r];
+                    else
+                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
+                }
+            }
+        }
+}
+
 }  // namespace
 
 hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
@@ -174,8 +454,15 @@ hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, in
                           hipStream_t stream) {
     const int tiles_m = (M + BM - 1) / BM;
     const int tiles_n = (N + BN - 1) / BN;
-    prefill_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(x, M, K, w, N, packed, alpha, y,
-                                                               y_dtype, tiles_m, tiles_n);
+    // the streaming kernel addresses x and W with 32-bit byte offsets
+    const bool stream_ok = K >= BK && K % BK == 0 && (int64_t)M * K < ((int64_t)1 << 31) &&
+                           (int64_t)N * K < ((int64_t)1 << 31);
+    if (stream_ok)
+        prefill_stream_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, y, y_dtype, tiles_m, tiles_n);
+    else
+        prefill_general_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, y, y_dtype, tiles_m, tiles_n);
     return hipGetLastError();
 }
 

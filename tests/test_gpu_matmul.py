@@ -121,8 +121,11 @@ def test_skinny_multi_ragged(M, N, K, T, yd):
         assert relf < 1e-5, relf
 
 
+# K a multiple of 64 selects the streaming kernel, other K the general one
 @pytest.mark.parametrize("M,N,K", [(65, 17, 32), (300, 520, 544), (513, 1000, 96),
-                                   (4, 256, 64), (256, 256, 256), (1000, 300, 4096)])
+                                   (4, 256, 64), (256, 256, 256), (1000, 300, 4096),
+                                   (300, 520, 576), (513, 1000, 128), (257, 255, 64),
+                                   (1, 300, 192), (600, 70, 640), (129, 513, 1088)])
 @pytest.mark.parametrize("yd", ["f32", "bf16"])
 def test_prefill_ragged(M, N, K, yd):
     p = wl.make_problem(M, N, K, 1, seed=M + N + K * 5, y_dtype=yd)
@@ -175,6 +178,26 @@ def test_one_hot_rows_every_bit_position(path):
     else:
         # the fused path rounds W + alpha*s to bf16 first
         np.testing.assert_allclose(y, ref, rtol=2.0 ** -8, atol=0)
+
+
+@pytest.mark.parametrize("K", [96, 128, 4096])
+def test_prefill_effective_weight_rounding_exact(K):
+    # x = e_k: y[k, n] is the fused path's effective weight itself, which is
+    # bf16_rne(fp32(W + s*alpha)); checked bit for bit on rows spanning the K tiles
+    N = 300
+    base = wl.make_problem(1, N, K, 1, seed=K + 1)
+    rows = np.unique(np.concatenate([np.arange(0, K, max(1, K // 160)), [K - 1]]))
+    x = np.zeros((len(rows), K), np.uint16)
+    x[np.arange(len(rows)), rows] = 0x3F80
+    p = wl.Problem("onehot-exact", x, base.w, base.alpha, packed=base.packed, y_dtype="f32")
+    log(f"effective-weight rounding K={K}")
+    y = host_out(run_matmul(p, path=PREFILL))
+    s = oracle.unpack(p.packed[0], K)[:, rows].T  # [rows, N] of +-1
+    wv = wl.bf16_bits_to_f32(p.w[:, rows].T)
+    a = np.float32(p.alpha[0])
+    eff = (wv + np.where(s > 0, a, -a).astype(np.float32)).astype(np.float32)
+    ref = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(eff))
+    assert np.array_equal(y, ref)
 
 
 @pytest.mark.parametrize("path", [SKINNY, PREFILL])
