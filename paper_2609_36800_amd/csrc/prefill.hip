@@ -224,9 +224,12 @@ typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2v;
 // One bf16 pair of effective weights, in two halves of four VALU operations
 // so that the work can be spread over two MFMA issue slots.  `s` carries the
 // chunk's eight sign bits twice (bit i and bit i+15); shifting by 15-2p
-// brings the bits of pair p to positions 15 and 31.  A clear bit (sign -1)
-// flips the sign of that weight, alpha is added in fp32, the sum is rounded to
-// bf16 (v_cvt_pk_bf16_f32, round to nearest even) and the flip is undone.
+// brings the bits of pair p to positions 15 and 31.  Where the bit is set
+// (sign +1) the weight's sign is flipped, -alpha is added in fp32, the sum is
+// rounded to bf16 (v_cvt_pk_bf16_f32, nearest even) and the flip is undone:
+// -bf16(-w - alpha) = bf16(w + alpha); where it is clear, w - alpha is rounded
+// directly.  The mask is hidden from the optimiser between its two uses so
+// each use folds into a single three-input bit operation.
 struct PairWork {
     uint32_t xm;
     float lo, hi;
@@ -234,27 +237,31 @@ struct PairWork {
 
 __device__ __forceinline__ PairWork fuse_pair_a(uint32_t w, uint32_t s, int p) {
     PairWork r;
-    r.xm = ~(s << (15 - 2 * p));
-    const uint32_t v = w ^ (r.xm & kSignBits);
+    const uint32_t xm = s << (15 - 2 * p);
+    const uint32_t v = opaque(w ^ (xm & kSignBits));
     r.lo = __builtin_bit_cast(float, v << 16);
     r.hi = __builtin_bit_cast(float, v & 0xFFFF0000u);
+    r.xm = opaque(xm);
     return r;
 }
 
-__device__ __forceinline__ uint32_t fuse_pair_b(const PairWork& q, float alpha) {
-    const f32x2v f = {q.lo + alpha, q.hi + alpha};
+__device__ __forceinline__ uint32_t fuse_pair_b(const PairWork& q, float neg_alpha) {
+    const f32x2v f = {q.lo + neg_alpha, q.hi + neg_alpha};
     const uint32_t r = __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
     return r ^ (q.xm & kSignBits);
 }
 
-__device__ __forceinline__ uint32_t fuse_pair(uint32_t w, uint32_t s, int p, float alpha) {
-    return fuse_pair_b(fuse_pair_a(w, s, p), alpha);
+__device__ __forceinline__ uint32_t fuse_pair(uint32_t w, uint32_t s, int p, float neg_alpha) {
+    return fuse_pair_b(fuse_pair_a(w, s, p), neg_alpha);
 }
 
+// YDT: output dtype; ALIGNED: output rows start on 16-byte boundaries (N a
+// multiple of 8 for bf16, of 4 for fp32), which allows 16-byte stores.
+template <int YDT, bool ALIGNED>
 __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha_p,
-    void* __restrict__ y, int y_dtype, int tiles_m, int tiles_n) {
+    void* __restrict__ y, int tiles_m, int tiles_n) {
     // Two buffers per operand, each [256 rows][64 k] bf16 = 32 KB.
     __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
     __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
@@ -270,7 +277,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const int wm = wv >> 1, wn = wv & 1;
     const int KT = K / BK;
     const int KW = K >> 5;
-    const float alpha = alpha_p[0];
+    const float neg_alpha = -alpha_p[0];
 
     // ---- staging assignment: per instruction i a wave moves rows
     //      32i + 8wv + (lane >> 3), lane l landing at LDS slot l & 7 ----
@@ -296,25 +303,32 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     for (int kk = 0; kk < 4; ++kk) rdo[kk] = (lane & 31) * BK + 8 * ((2 * kk + (lane >> 5)) ^ frd);
     const int a_row0 = wm * 128 * BK, b_row0 = wn * 128 * BK;
 
-    const char* xg = reinterpret_cast<const char*>(x);
-    const char* wg = reinterpret_cast<const char*>(w);
-    const char* sg = reinterpret_cast<const char*>(packed);
+    // Buffer resources: per-lane 32-bit byte offsets (row and chunk) plus a
+    // wave-uniform k-tile offset in an SGPR, so no address arithmetic is
+    // spent per load.  Row indices are clamped, so every access is in range.
+    constexpr int kRawBufferFlags = 0x00020000;  // untyped 32-bit data format
+    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(x), (short)0, (int)((uint32_t)M * (uint32_t)K * 2u), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(w), (short)0, (int)((uint32_t)N * (uint32_t)K * 2u), kRawBufferFlags);
+    const __amdgpu_buffer_rsrc_t sres = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint32_t*>(packed), (short)0, (int)((uint32_t)N * (uint32_t)KW * 4u), kRawBufferFlags);
 
     auto load_w = [&](u32x4& dst, int i, int kt) {
-        dst = *reinterpret_cast<const u32x4*>(wg + (size_t)kt * (BK * 2) + woff[i]);
+        dst = __builtin_amdgcn_raw_buffer_load_b128(wres, (int)woff[i], kt * (BK * 2), 0);
     };
     auto load_s = [&](uint32_t& dst, int i, int kt) {
-        dst = *reinterpret_cast<const uint32_t*>(sg + (size_t)kt * 8 + soff[i]);
+        dst = __builtin_amdgcn_raw_buffer_load_b32(sres, (int)soff[i], kt * 8, 0);
     };
-    auto copy_x = [&](uint16_t* dst, int kt) {
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            __builtin_amdgcn_global_load_lds(xg + (size_t)kt * (BK * 2) + xoff[i],
-                                             dst + (32 * i + 8 * wv) * BK, 16, 0, 0);
+    auto load_x = [&](u32x4& dst, int i, int kt) {
+        dst = __builtin_amdgcn_raw_buffer_load_b128(xres, (int)xoff[i], kt * (BK * 2), 0);
     };
     auto sign_word = [&](uint32_t d) {
         const uint32_t byte = (d >> sbit) & 0xFFu;
         return opaque(byte | (byte << 15));
+    };
+    auto frag = [&](const uint16_t* buf, int row0, int blk, int kk) {
+        return *reinterpret_cast<const u32x4*>(buf + row0 + blk * 32 * BK + rdo[kk]);
     };
 
     f32x16 acc[4][4];
@@ -325,126 +339,206 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    // Register sets of raw W / sign words: set (t & 1) holds tile t + 2 while
-    // tile t is multiplied... precisely, iteration t decodes set (t + 1) & 1
-    // (tile t + 1) and refills it with tile t + 3.
+    // Raw W / sign-word register sets.  Chunk c of the tile decoded in the
+    // second half of the decode stream... concretely: body t decodes chunks
+    // 2..7 of tile t+1 (set (t+1)&1) and chunks 0..1 of tile t+2 (set t&1),
+    // and refills every chunk it consumed with the tile two further on.
     u32x4 w0[8], w1[8];
     uint32_t s0[8], s1[8];
 
-    // ---- prologue: tile 0 decoded into sB0, x tile 0 copied, tiles 1, 2 loaded ----
+    // ---- prologue: tile 0 and chunks 0..1 of tile 1 staged, registers primed ----
+    u32x4 xr[8];
+    const int k1 = min(1, KT - 1), k2 = min(2, KT - 1), k3 = min(3, KT - 1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, 0); load_s(s0[i], i, 0); }
-    copy_x(sA0, 0);
+    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, 0); load_s(s0[i], i, 0); load_x(xr[i], i, 0); }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { load_w(w1[i], i, min(1, KT - 1)); load_s(s1[i], i, min(1, KT - 1)); }
+    for (int i = 0; i < 8; ++i) { load_w(w1[i], i, k1); load_s(s1[i], i, k1); }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        const uint32_t s = sign_word(s0[i]);
+        *reinterpret_cast<u32x4*>(sA0 + i * 32 * BK + st_lane) = xr[i];
+        const uint32_t sw0 = sign_word(s0[i]);
         u32x4 o;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w0[i][p], s, p, alpha);
+        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w0[i][p], sw0, p, neg_alpha);
         *reinterpret_cast<u32x4*>(sB0 + i * 32 * BK + st_lane) = o;
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, min(2, KT - 1)); load_s(s0[i], i, min(2, KT - 1)); }
+    for (int i = 0; i < 8; ++i) { load_x(xr[i], i, k1); load_w(w0[i], i, k2); load_s(s0[i], i, k2); }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        *reinterpret_cast<u32x4*>(sA1 + i * 32 * BK + st_lane) = xr[i];
+        const uint32_t sw1 = sign_word(s1[i]);
+        u32x4 o;
+#pragma unroll
+        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w1[i][p], sw1, p, neg_alpha);
+        *reinterpret_cast<u32x4*>(sB1 + i * 32 * BK + st_lane) = o;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) { load_x(xr[i], i, k2); load_w(w1[i], i, k3); load_s(s1[i], i, k3); }
+    uint32_t sw = sign_word(s1[2]);
+    raw_barrier();
+    u32x4 fa[4], fb[4], na[4], nb[4];
+    fa[0] = frag(sA0, a_row0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) fb[j] = frag(sB0, b_row0, j, 0);
+#pragma unroll
+    for (int i = 1; i < 4; ++i) fa[i] = frag(sA0, a_row0, i, 0);
 
-    auto step = [&](auto par, int t) {
+    // Body t: the 64 MFMAs of tile t.  Fragments are always read one k-step
+    // ahead, so the barrier that publishes tile t+1 sits between k-steps 2
+    // and 3: by then every read of tile t has been issued and waited for, the
+    // buffers of tile t are free for tile t+2, and k-step 3 overlaps the reads
+    // of tile t+1's first fragments.  Slot g (0..63) also carries position
+    // p of the decode stream: g < 48 -> chunks 2..7 of tile t+1 (p = g+16),
+    // g >= 48 -> chunks 0..1 of tile t+2 (p = g-48); chunk p/8, step p%8:
+    // even steps form half a pair, odd steps finish it; step 6 refills the
+    // sign word, step 7 writes the chunk to LDS and refills its raw weights.
+    auto body = [&](auto par, int t) {
         constexpr int P = decltype(par)::value;
         uint16_t* const Ac = P ? sA1 : sA0;
         uint16_t* const An = P ? sA0 : sA1;
         uint16_t* const Bc = P ? sB1 : sB0;
         uint16_t* const Bn = P ? sB0 : sB1;
-        u32x4(&ws)[8] = pick<P ^ 1>(w0, w1);
-        uint32_t(&ss)[8] = pick<P ^ 1>(s0, s1);
+        u32x4(&wn1)[8] = pick<P ^ 1>(w0, w1);      // tile t+1
+        uint32_t(&sn1)[8] = pick<P ^ 1>(s0, s1);
+        u32x4(&wn2)[8] = pick<P>(w0, w1);          // tile t+2
+        uint32_t(&sn2)[8] = pick<P>(s0, s1);
+        const int kr1 = min(t + 3, KT - 1), kr2 = min(t + 4, KT - 1);
+        const int kx1 = min(t + 2, KT - 1), kx2 = min(t + 3, KT - 1);
 
-        // x tile t and the raw W of tile t + 1 were issued before the last 16
-        // loads (the W/sign loads of the previous iteration); this wave's LDS
-        // writes of tile t are done.  The barrier publishes both to all waves.
-        asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-
-        u32x4 fa[4], fb[4], na[4], nb[4];
-        // read order a0 b0 b1 b2 b3 a1 a2 a3 follows the MFMA order below, so
-        // the first MFMA waits for two reads only
-        fa[0] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + rdo[0]);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            fb[j] = *reinterpret_cast<const u32x4*>(Bc + b_row0 + j * 32 * BK + rdo[0]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-#pragma unroll
-        for (int i = 1; i < 4; ++i) {
-            fa[i] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + i * 32 * BK + rdo[0]);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        copy_x(An, min(t + 1, KT - 1));
-        const int kw = min(t + 3, KT - 1);
-        uint32_t sw = sign_word(ss[0]);
-        __builtin_amdgcn_sched_barrier(0);
-
-        // Slot g = 16kk + m issues MFMA (m / 4, m % 4) of k-step kk and half a
-        // pair of chunk c = g / 8: u = g % 8 even -> first half of pair u / 2,
-        // odd -> second half.  Chunk c is written to LDS in the slot after its
-        // last half; its registers are refilled with tile t + 3 once consumed.
         PairWork pw;
-        u32x4 o, o_prev;
+        u32x4 o;
+        uint32_t sw_next = 0;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
+        for (int b = 0; b < 4; ++b) {
+            if (b == 3) {
+                // this wave's LDS writes of tile t+1 are complete; publish them
+                raw_barrier();
+                __builtin_amdgcn_sched_barrier(0);
+            }
 #pragma unroll
             for (int m = 0; m < 16; ++m) {
                 const int i = m >> 2, j = m & 3;
-                acc[i][j] = mfma32(fa[i], fb[j], acc[i][j]);
-                if (kk < 3 && m < 8) {
-                    if (m == 0) na[0] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + rdo[kk + 1]);
-                    else if (m < 5) nb[m - 1] = *reinterpret_cast<const u32x4*>(Bc + b_row0 + (m - 1) * 32 * BK + rdo[kk + 1]);
-                    else na[m - 4] = *reinterpret_cast<const u32x4*>(Ac + a_row0 + (m - 4) * 32 * BK + rdo[kk + 1]);
+                acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
+                if (m < 8) {
+                    const uint16_t* abuf = b < 3 ? Ac : An;
+                    const uint16_t* bbuf = b < 3 ? Bc : Bn;
+                    const int kk = b < 3 ? b + 1 : 0;
+                    if (m == 0) na[0] = frag(abuf, a_row0, 0, kk);
+                    else if (m < 5) nb[m - 1] = frag(bbuf, b_row0, m - 1, kk);
+                    else na[m - 4] = frag(abuf, a_row0, m - 4, kk);
                 }
-                const int g = kk * 16 + m, c = g >> 3, u = g & 7;
-                if (u == 0 && c > 0) *reinterpret_cast<u32x4*>(Bn + (c - 1) * 32 * BK + st_lane) = o_prev;
+                const int g = b * 16 + m;
+                const bool first = g < 48;
+                const int pos = first ? g + 16 : g - 48;
+                const int c = pos >> 3, u = pos & 7;
+                u32x4(&ws)[8] = first ? wn1 : wn2;
+                uint32_t(&ss)[8] = first ? sn1 : sn2;
+                uint16_t* const dst = first ? Bn : Bc;
+                uint16_t* const xdst = first ? An : Ac;
+                const int kr = first ? kr1 : kr2;
+                const int kx = first ? kx1 : kx2;
                 if ((u & 1) == 0) pw = fuse_pair_a(ws[c][u >> 1], sw, u >> 1);
-                else o[u >> 1] = fuse_pair_b(pw, alpha);
-                if (u == 6) load_s(ss[c], c, kw);
-                if (u == 7) {
-                    load_w(ws[c], c, kw);
-                    if (c < 7) sw = sign_word(ss[c + 1]);
-                    o_prev = o;
+                else o[u >> 1] = fuse_pair_b(pw, neg_alpha);
+                if (u == 6) {
+                    // sign word of the next chunk in stream order
+                    sw_next = c < 7 ? sign_word(ss[c + 1]) : sign_word(sn2[0]);
+                    load_s(ss[c], c, kr);
                 }
-                if (g == 63) *reinterpret_cast<u32x4*>(Bn + 7 * 32 * BK + st_lane) = o;
+                if (u == 7) {
+                    *reinterpret_cast<u32x4*>(dst + c * 32 * BK + st_lane) = o;
+                    *reinterpret_cast<u32x4*>(xdst + c * 32 * BK + st_lane) = xr[c];
+                    load_w(ws[c], c, kr);
+                    load_x(xr[c], c, kx);
+                    sw = sw_next;
+                }
                 __builtin_amdgcn_sched_barrier(0);
             }
-            if (kk < 3) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) { fa[r] = na[r]; fb[r] = nb[r]; }
-            }
+            for (int r = 0; r < 4; ++r) { fa[r] = na[r]; fb[r] = nb[r]; }
         }
     };
 
     int t = 0;
     for (; t + 1 < KT; t += 2) {
-        step(std::integral_constant<int, 0>{}, t);
-        step(std::integral_constant<int, 1>{}, t + 1);
+        body(std::integral_constant<int, 0>{}, t);
+        body(std::integral_constant<int, 1>{}, t + 1);
     }
-    if (t < KT) step(std::integral_constant<int, 0>{}, t);
-    // copies issued for tiles past the end still target LDS: drain them
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (t < KT) body(std::integral_constant<int, 0>{}, t);
 
-    // ---- epilogue: lane holds column (lane & 31) of each 32x32 tile ----
+    // ---- epilogue.  The W fragment is the MFMA's first operand, so acc[i][j][r]
+    //      holds y[mrow + 32i][ncol + 32j + 8(r >> 2) + (r & 3)]: four
+    //      consecutive columns per register quad ----
+    const int mrow = m0 + wm * 128 + (lane & 31);
+    const int ncol = n0 + wn * 128 + 4 * (lane >> 5);
+    if constexpr (YDT == kBF16 && ALIGNED) {
+        // Rows go through LDS, 64 at a time, so that each lane stores 16
+        // contiguous bytes and a store instruction covers whole 256-byte rows.
+        raw_barrier();  // every wave is done with the operand buffers
+        uint16_t* const stage = wv == 0 ? sA0 : wv == 1 ? sA1 : wv == 2 ? sB0 : sB1;
+        constexpr int kStageRow = 136;  // bf16 per staged row: 128 + 8 padding
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int half = 0; half < 2; ++half) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int col = n0 + wn * 128 + j * 32 + (lane & 31);
+            for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (row < M && col < N) {
-                    if (y_dtype == kF32)
-                        reinterpret_cast<float*>(y)[(size_t)row * N + col] = acc[i][j][r];
-                    else
-                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
-                }
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int i = 2 * half + ii;
+                        const f32x2v lo = {acc[i][j][4 * q], acc[i][j][4 * q + 1]};
+                        const f32x2v hi = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                        uint2 v;
+                        v.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2v));
+                        v.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2v));
+                        *reinterpret_cast<uint2*>(stage + (32 * ii + (lane & 31)) * kStageRow + 32 * j +
+                                                  8 * q + 4 * (lane >> 5)) = v;
+                    }
+            // each wave reads back only rows it wrote itself
+#pragma unroll
+            for (int t = 0; t < 16; ++t) {
+                const int qd = lane + 64 * t, row = qd >> 4, c8 = qd & 15;
+                const u32x4 v = *reinterpret_cast<const u32x4*>(stage + row * kStageRow + c8 * 8);
+                const int gm = m0 + wm * 128 + 64 * half + row, gn = n0 + wn * 128 + c8 * 8;
+                if (gm < M && gn < N)
+                    *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(y) + (size_t)gm * N + gn) = v;
             }
         }
+    } else if constexpr (YDT == kF32) {
+        constexpr bool vec = ALIGNED;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int row = mrow + 32 * i, col = ncol + 32 * j + 8 * q;
+                    if (row >= M) continue;
+                    float* dst = reinterpret_cast<float*>(y) + (size_t)row * N + col;
+                    if constexpr (vec) {
+                        if (col >= N) continue;
+                        const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                         acc[i][j][4 * q + 3]};
+                        *reinterpret_cast<f32x4*>(dst) = v;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (col + e < N) dst[e] = acc[i][j][4 * q + e];
+                    }
+                }
+    } else {
+        // bf16 rows not 16-byte aligned: element stores
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int row = mrow + 32 * i, col = ncol + 32 * j + 8 * (r >> 2) + (r & 3);
+                    if (row < M && col < N)
+                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
+                }
+    }
 }
 
 }  // namespace
@@ -454,12 +548,19 @@ hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, in
                           hipStream_t stream) {
     const int tiles_m = (M + BM - 1) / BM;
     const int tiles_n = (N + BN - 1) / BN;
-    // the streaming kernel addresses x and W with 32-bit byte offsets
-    const bool stream_ok = K >= BK && K % BK == 0 && (int64_t)M * K < ((int64_t)1 << 31) &&
-                           (int64_t)N * K < ((int64_t)1 << 31);
-    if (stream_ok)
-        prefill_stream_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, y, y_dtype, tiles_m, tiles_n);
+    // the streaming kernel addresses x and W through buffer resources whose
+    // byte extents must fit in 31 bits
+    const bool stream_ok = K >= BK && K % BK == 0 && (int64_t)M * K < ((int64_t)1 << 30) &&
+                           (int64_t)N * K < ((int64_t)1 << 30);
+    const dim3 grid(tiles_m * tiles_n), block(kThreads);
+    if (stream_ok && y_dtype == kBF16 && N % 8 == 0)
+        prefill_stream_kernel<kBF16, true><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
+    else if (stream_ok && y_dtype == kBF16)
+        prefill_stream_kernel<kBF16, false><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
+    else if (stream_ok && N % 4 == 0)
+        prefill_stream_kernel<kF32, true><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
+    else if (stream_ok)
+        prefill_stream_kernel<kF32, false><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
     else
         prefill_general_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(
             x, M, K, w, N, packed, alpha, y, y_dtype, tiles_m, tiles_n);
