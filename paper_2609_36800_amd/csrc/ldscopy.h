@@ -40,4 +40,12 @@ __device__ __forceinline__ void copy16_to_lds(const void* src, void* lds_base) {
                  :: "s"(lds_off), "v"(src) : "memory", "m0");
 }
 
+// One 4-byte-per-lane copy global -> LDS: lane l's word lands at
+// lds_base + 4*l (256 bytes per wave).
+__device__ __forceinline__ void copy4_to_lds(const void* src, void* lds_base) {
+    const uint32_t lds_off = (uint32_t)(uintptr_t)(lds_void*)lds_base;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, off"
+                 :: "s"(lds_off), "v"(src) : "memory", "m0");
+}
+
 }  // namespace bitdelta
