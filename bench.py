@@ -284,6 +284,59 @@ def pmc_pass(steps):
                       "kernel_source_hash": kernel_source_hash()}), flush=True)
 
 
+def traffic_from(fetch_dir, write_dir, out_path):
+    """Turn the two rocprofv3 --pmc runs of `--pmc-pass` (FETCH_SIZE, then
+    WRITE_SIZE, in KiB per dispatch) into HBM bytes per headline launch.  Each
+    counter is scaled by what it reads for the 512 MiB calibration copy that
+    the same run performs (known bytes read and written)."""
+    import csv
+    import glob
+    import statistics
+
+    def per_dispatch(d, counter):
+        vals, names = {}, {}
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            for r in csv.DictReader(open(f)):
+                if r["Counter_Name"] != counter:
+                    continue
+                key = r["Dispatch_Id"]
+                vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+                names[key] = r["Kernel_Name"]
+        return vals, names
+
+    copy_bytes = 512 << 20
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        vals, names = per_dispatch(d, counter)
+        lib = [v for k, v in vals.items() if "bitdelta" in names[k] and "decode" in names[k]]
+        copies = [v for k, v in vals.items() if "bitdelta" not in names[k] and v * 1024 > copy_bytes / 4]
+        if not lib or not copies:
+            raise SystemExit(f"{counter}: no library or calibration-copy dispatches found in {d}")
+        raw = statistics.mean(lib)
+        scale = copy_bytes / (statistics.median(copies[-3:]) * 1024)
+        out[counter] = (raw, scale)
+    hbm = out["FETCH_SIZE"][0] * 1024 * out["FETCH_SIZE"][1] + out["WRITE_SIZE"][0] * 1024 * out["WRITE_SIZE"][1]
+    alg = (algorithmic_bytes(1, 4096, 4096, 1) + algorithmic_bytes(16, 4096, 4096, 1)) / 2
+    rec = {
+        "kernel": "stream_decode_kernel (M=1 and M=16 launches alternating, N=K=4096)",
+        "kernel_source_hash": kernel_source_hash(),
+        "fetch_kib_per_launch_raw": round(out["FETCH_SIZE"][0], 1),
+        "write_kib_per_launch_raw": round(out["WRITE_SIZE"][0], 1),
+        "fetch_scale_from_copy": round(out["FETCH_SIZE"][1], 4),
+        "write_scale_from_copy": round(out["WRITE_SIZE"][1], 4),
+        "hbm_bytes_per_launch": int(round(hbm)),
+        "algorithmic_bytes_per_launch": alg,
+        "commands": [
+            "rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch_dir> -o run -- python3 bench.py --pmc-pass --steps 64",
+            "rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write_dir> -o run -- python3 bench.py --pmc-pass --steps 64",
+            "python3 bench.py --traffic-from <fetch_dir> <write_dir>",
+        ],
+    }
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -294,7 +347,14 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only launch the headline kernels and a calibration copy (for rocprofv3 --pmc)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write the HBM traffic record from two --pmc runs of --pmc-pass (no GPU needed)")
     args = ap.parse_args()
+
+    if args.traffic_from:
+        traffic_from(args.traffic_from[0], args.traffic_from[1],
+                     os.path.join(ROOT, "profiles", "decode_gemv_4096x4096_traffic.json"))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -324,7 +384,7 @@ def main():
     achieved = per_launch_bytes / avg_launch_s / 1e9
     roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": achieved / HBM_PEAK_GBS, "traffic": recorded_traffic(),
-                "kernel": "decode_kernel (single tenant, M <= 16)",
+                "kernel": "stream_decode_kernel (single tenant, M <= 16)",
                 "per_launch_bytes": per_launch_bytes,
                 "avg_launch_us": head["avg_launch_us"]}
 
