@@ -134,6 +134,19 @@ def test_prefill_ragged(M, N, K, yd):
     check(y, oracle_y(p), p.x, p.w, p.alpha)
 
 
+# more distinct tenants than one pass of the batched kernel holds (16 slots up
+# to 32 rows, 8 above): later passes re-stream x and signs and skip the base
+@pytest.mark.parametrize("M,N,K,T", [(32, 150, 384, 32), (48, 200, 512, 40), (64, 130, 256, 64),
+                                     (20, 70, 1024, 20), (33, 16, 128, 33)])
+def test_multi_tenant_several_passes(M, N, K, T):
+    p = wl.make_problem(M, N, K, T, seed=M * 3 + T, multi_tenant=True, y_dtype="f32")
+    p.tenant_ids = np.random.default_rng(M + T).permutation(np.arange(M) % T).astype(np.int32)
+    log(f"multi-tenant passes M={M} N={N} K={K} T={T} distinct={len(np.unique(p.tenant_ids))}")
+    y = host_out(run_matmul(p))
+    relf, _ = check(y, oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    assert relf < 1e-5, relf
+
+
 def test_skinny_forced_above_64_rows():
     p = wl.make_problem(150, 70, 256, 1, seed=3, y_dtype="f32")
     log("skinny forced M=150")
