@@ -66,11 +66,12 @@ class Launcher:
         return call
 
 
-def make_sets(count, M, N, K, T, multi, seed, dev):
+def make_sets(count, M, N, K, T, multi, seed, dev, prompts=0):
     import workloads as wl
     sets = []
     for i in range(count):
-        d = wl.device_problem(M, N, K, T, multi_tenant=multi, seed=seed + i, device=dev)
+        d = wl.device_problem(M, N, K, T, multi_tenant=multi, seed=seed + i, device=dev,
+                              prompts=prompts)
         sets.append(d)
     return sets
 
@@ -117,7 +118,7 @@ def timed(replay, reps):
 
 
 def bench_workload(name, shapes, T, multi, flops_fn, steps, warmup, dev, launcher, seed,
-                   rotate=True):
+                   rotate=True, prompts=0):
     """Time exactly `steps` steps; a step is one launch per (M, N, K) in `shapes`.
 
     With rotate, consecutive launches read different buffer sets and the sets
@@ -132,7 +133,7 @@ def bench_workload(name, shapes, T, multi, flops_fn, steps, warmup, dev, launche
     for r in range(nrot):
         step_calls, b = [], 0
         for j, (M, N, K) in enumerate(shapes):
-            d = make_sets(1, M, N, K, T, multi, seed + 1000 * j + r, dev)[0]
+            d = make_sets(1, M, N, K, T, multi, seed + 1000 * j + r, dev, prompts)[0]
             y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
             used = 1 if d["tenant_ids"] is None else len(np.unique(d["tenant_ids"].cpu().numpy()))
             b += algorithmic_bytes(M, N, K, used)
@@ -400,6 +401,15 @@ def main():
             20, args.warmup, dev, launcher, seed=90, rotate=False)
         pf["mfma_frac"] = pf["TFLOPs"] / BF16_PEAK_TFLOPS
         workloads.append(pf)
+        import workloads as wl
+        c = wl.MT_PREFILL
+        mpf = bench_workload(
+            "multi-tenant prefill: x 4096x4096 as 16 prompts of random length, one tenant per "
+            "prompt drawn from 8, W_base 4096x4096, grouped fused bf16 GEMM",
+            [(c["M"], c["N"], c["K"])], c["T"], True, lambda M, N, K: 2 * M * N * K,
+            20, args.warmup, dev, launcher, seed=130, rotate=False, prompts=c["prompts"])
+        mpf["mfma_frac"] = mpf["TFLOPs"] / BF16_PEAK_TFLOPS
+        workloads.append(mpf)
         workloads.append(llama_sweep(dev, launcher, args.warmup))
 
     cpu = None if args.no_cpu else cpu_baseline(args.cpu_budget)

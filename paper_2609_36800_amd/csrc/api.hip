@@ -10,6 +10,10 @@
 namespace {
 
 constexpr int kSkinnyRows = 64;
+// Batched requests with at least this many rows take the grouped fused GEMM
+// (one pass over W per output tile) rather than the decode-shaped kernel,
+// which streams W once per 64 rows.
+constexpr int kGroupedMinRows = 256;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -54,9 +58,13 @@ int check_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w, int
     return BITDELTA_OK;
 }
 
-int choose_path(int64_t M, int has_tenant_ids) {
-    if (has_tenant_ids || M <= kSkinnyRows) return BITDELTA_PATH_SKINNY;
-    return BITDELTA_PATH_PREFILL;
+int choose_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
+    if (M <= kSkinnyRows) return BITDELTA_PATH_SKINNY;
+    if (!has_tenant_ids) return BITDELTA_PATH_PREFILL;
+    if (M >= kGroupedMinRows && M <= kMaxDim && N <= kMaxDim && K <= kMaxDim &&
+        bitdelta::prefill_grouped_supported((int)M, (int)N, (int)K, T))
+        return BITDELTA_PATH_PREFILL;
+    return BITDELTA_PATH_SKINNY;
 }
 
 }  // namespace
@@ -106,10 +114,7 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K, void* signs
 }
 
 int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
-    (void)N;
-    (void)K;
-    (void)T;
-    return choose_path(M, has_tenant_ids);
+    return choose_path(M, N, K, T, has_tenant_ids);
 }
 
 int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
@@ -118,11 +123,17 @@ int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uin
                               int path, hipStream_t stream) {
     int rc = check_matmul(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, y, y_dtype);
     if (rc != BITDELTA_OK) return rc;
-    if (path == BITDELTA_PATH_AUTO) path = choose_path(M, tenant_ids != nullptr);
+    if (path == BITDELTA_PATH_AUTO) path = choose_path(M, N, K, T, tenant_ids != nullptr);
     if (path != BITDELTA_PATH_SKINNY && path != BITDELTA_PATH_PREFILL) return BITDELTA_ERR_UNSUPPORTED;
-    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr) return BITDELTA_ERR_UNSUPPORTED;
+    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr &&
+        !bitdelta::prefill_grouped_supported((int)M, (int)N, (int)K, T))
+        return BITDELTA_ERR_UNSUPPORTED;
     if (M == 0 || N == 0) return BITDELTA_OK;
 
+    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr)
+        return hip_status(bitdelta::launch_prefill_grouped(x, (int)M, (int)K, w_base, (int)N,
+                                                           packed_s, alpha, tenant_ids, (int)T, y,
+                                                           y_dtype, stream));
     if (path == BITDELTA_PATH_PREFILL)
         return hip_status(bitdelta::launch_prefill(x, (int)M, (int)K, w_base, (int)N, packed_s,
                                                    alpha, y, y_dtype, stream));

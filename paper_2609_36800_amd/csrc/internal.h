@@ -38,8 +38,17 @@ hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int
                          hipStream_t stream);
 
 // Prefill-shaped single-tenant matmul: one bf16 GEMM over W + alpha*s.
+bool prefill_stream_supported(int M, int N, int K);
 hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                           const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                           hipStream_t stream);
+
+// Prefill-shaped batched matmul: one fused GEMM per tenant over its rows,
+// routed on the device; needs prefill_grouped_supported.
+bool prefill_grouped_supported(int M, int N, int K, int T);
+hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                                  const uint32_t* packed, const float* alpha,
+                                  const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                                  hipStream_t stream);
 
 }  // namespace bitdelta

@@ -192,11 +192,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
 
 // ------------------------------------------------------------ streaming kernel
 
-// Output-tile assignment shared by both kernels (XCD-aware, groups of kGroupM
-// tile rows).
-__device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tile_m, int& tile_n) {
+// Output-tile assignment (XCD-aware, groups of kGroupM tile rows) of block
+// `bid` < tiles_m * tiles_n.
+__device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& tile_m, int& tile_n) {
     const int nwg = tiles_m * tiles_n;
-    int bid = blockIdx.x;
     if ((nwg & 7) == 0) bid = (bid & 7) * (nwg >> 3) + (bid >> 3);
     const int group = bid / (kGroupM * tiles_n);
     const int first_m = group * kGroupM;
@@ -204,6 +203,145 @@ __device__ __forceinline__ void tile_of(int tiles_m, int tiles_n, int& tile_m, i
     const int local = bid - group * kGroupM * tiles_n;
     tile_m = first_m + local % gm;
     tile_n = local / gm;
+}
+
+// ---------------------------------------------------- batched (grouped) form
+//
+// With a tenant id per row the fused GEMM runs once per tenant over that
+// tenant's rows (the batched BitDelta GEMM of Section 4.4): the rows of tenant
+// t, in increasing row order, form ceil(c_t / 256) row tiles, numbered tenant
+// by tenant, and each output tile decodes its own tenant's effective weights.
+// Every workgroup routes the rows itself, so no scratch memory and no extra
+// launch are needed: it histograms the ids (one histogram per wave over a
+// quarter of the rows, in LDS that the operand buffers reuse afterwards),
+// scans the per-tenant tile counts, picks its tile from its block index (the
+// number of tiles is known only on the device, so the grid covers the upper
+// bound and surplus workgroups leave), and collects its tile's row indices.
+constexpr int kMaxGroupedTenants = BM * BK * 2 / (4 * 4);  // 4 histograms of T ints in 32 KB
+
+// Returns false (for the whole workgroup) when block `bid` owns no tile;
+// else `tenant`, `tile_n` and rows[0..255] (row index, -1 past the tenant's
+// last row).  hist: 4*T ints of LDS; info: 8 ints of LDS.
+__device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int tiles_n, int bid,
+                           int* hist, int* rows, int* info, int& tenant, int& tile_n) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int seg = ((M + 255) >> 8) << 6;  // rows per wave, a multiple of 64
+    const int r_beg = min(M, seg * wv), r_end = min(M, seg * (wv + 1));
+
+    int* h = hist + wv * T;
+    for (int i = lane; i < T; i += 64) h[i] = 0;
+    __syncthreads();
+    for (int base = r_beg; base < r_end; base += 512) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int m = base + 64 * u + lane;
+            v[u] = m < r_end ? ids[m] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if ((unsigned)v[u] < (unsigned)T) atomicAdd(&h[v[u]], 1);
+    }
+    __syncthreads();
+
+    // tiles per tenant; exclusive scan over tenants (thread i takes a run of them)
+    const int per = (T + kThreads - 1) / kThreads;
+    const int t_beg = min(T, tid * per), t_end = min(T, t_beg + per);
+    auto count = [&](int t) { return hist[t] + hist[T + t] + hist[2 * T + t] + hist[3 * T + t]; };
+    int s = 0;
+    for (int t = t_beg; t < t_end; ++t) s += (count(t) + BM - 1) / BM;
+    int incl = s;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int o = __shfl_up(incl, d);
+        if (lane >= d) incl += o;
+    }
+    if (lane == 63) info[wv] = incl;
+    __syncthreads();
+    const int total = info[0] + info[1] + info[2] + info[3];
+    int excl = incl - s;
+    for (int w2 = 0; w2 < wv; ++w2) excl += info[w2];
+    if (bid >= total * tiles_n) return false;
+    int tile_v;
+    tile_of(bid, total, tiles_n, tile_v, tile_n);
+    if (tile_v >= excl && tile_v < excl + s) {
+        int first = excl;
+        for (int t = t_beg; t < t_end; ++t) {
+            const int nt = (count(t) + BM - 1) / BM;
+            if (tile_v < first + nt) {
+                info[4] = t;
+                info[5] = tile_v - first;
+                break;
+            }
+            first += nt;
+        }
+    }
+    rows[tid] = -1;
+    __syncthreads();
+
+    // rank of each row among its tenant's rows: this wave's base from the
+    // earlier waves' histograms, then ballots over 64-row chunks in order
+    const int t = info[4], lo = info[5] * BM;
+    int rank = 0;
+    for (int w2 = 0; w2 < wv; ++w2) rank += hist[w2 * T + t];
+    for (int base = r_beg; base < r_end && rank < lo + BM; base += 512) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const int m = base + 64 * u + lane;
+            v[u] = m < r_end ? ids[m] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint64_t mask = __ballot(v[u] == t);
+            if (v[u] == t) {
+                const int below = (int)__builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                const int r = rank + below - lo;
+                if (r >= 0 && r < BM) rows[r] = base + 64 * u + lane;
+            }
+            rank += __popcll(mask);
+        }
+    }
+    __syncthreads();
+    tenant = t;
+    return true;
+}
+
+// Rows whose tenant id lies outside [0, T) are written as quiet NaN, columns
+// [n0, n0 + 256) (one workgroup per column tile).
+template <int YDT>
+__device__ void write_invalid_rows(const int32_t* __restrict__ ids, int M, int T, int N, int n0,
+                                   void* __restrict__ y) {
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int base = 64 * wv; base < M; base += 4 * 64 * 4) {
+        int v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int m = base + 256 * u + lane;
+            v[u] = m < M ? ids[m] : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int m = base + 256 * u + lane;
+            uint64_t mask = __ballot(m < M && (unsigned)v[u] >= (unsigned)T);
+            while (mask) {
+                const int r = base + 256 * u + __builtin_ctzll(mask);
+                mask &= mask - 1;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int col = n0 + 4 * lane + e;
+                    if (col >= N) continue;
+                    if constexpr (YDT == kF32)
+                        reinterpret_cast<float*>(y)[(size_t)r * N + col] = __builtin_nanf("");
+                    else
+                        reinterpret_cast<uint16_t*>(y)[(size_t)r * N + col] = to_bf16(__builtin_nanf(""));
+                }
+            }
+        }
+    }
 }
 
 template <int P, class T>
@@ -257,27 +395,53 @@ __device__ __forceinline__ uint32_t fuse_pair(uint32_t w, uint32_t s, int p, flo
 
 // YDT: output dtype; ALIGNED: output rows start on 16-byte boundaries (N a
 // multiple of 8 for bf16, of 4 for fp32), which allows 16-byte stores.
-template <int YDT, bool ALIGNED>
+// GROUPED: the batched form (tenant id per row, at most kMaxGroupedTenants
+// tenants); tiles_m is then the upper bound on the number of row tiles, and
+// tiles_n more workgroups past tiles_m * tiles_n write the rows of invalid ids.
+template <int YDT, bool ALIGNED, bool GROUPED>
 __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha_p,
-    void* __restrict__ y, int tiles_m, int tiles_n) {
+    const int32_t* __restrict__ ids, int T, void* __restrict__ y, int tiles_m, int tiles_n) {
     // Two buffers per operand, each [256 rows][64 k] bf16 = 32 KB.
     __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
     __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
     __shared__ __attribute__((aligned(1024))) uint16_t sB0[BN * BK];
     __shared__ __attribute__((aligned(1024))) uint16_t sB1[BN * BK];
+    __shared__ int sRows[GROUPED ? BM : 1];   // global row of each tile row, -1 = none
+    __shared__ int sInfo[GROUPED ? 8 : 1];
 
-    int tile_m, tile_n;
-    tile_of(tiles_m, tiles_n, tile_m, tile_n);
+    int tile_m = 0, tile_n, tenant = 0;
+    if constexpr (GROUPED) {
+        if ((int)blockIdx.x >= tiles_m * tiles_n) {
+            write_invalid_rows<YDT>(ids, M, T, N, ((int)blockIdx.x - tiles_m * tiles_n) * BN, y);
+            return;
+        }
+        if (!route_rows(ids, M, T, tiles_n, blockIdx.x, reinterpret_cast<int*>(sA0), sRows, sInfo,
+                        tenant, tile_n))
+            return;
+    } else {
+        tile_of(blockIdx.x, tiles_m, tiles_n, tile_m, tile_n);
+    }
     const int m0 = tile_m * BM, n0 = tile_n * BN;
+    // global row g of tile row lr; false when the tile row holds no row
+    auto out_row = [&](int lr, int& g) -> bool {
+        if constexpr (GROUPED) {
+            g = sRows[lr];
+            return g >= 0;
+        } else {
+            g = m0 + lr;
+            return g < M;
+        }
+    };
 
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wv >> 1, wn = wv & 1;
     const int KT = K / BK;
     const int KW = K >> 5;
-    const float neg_alpha = -alpha_p[0];
+    const float neg_alpha = -alpha_p[tenant];
+    packed += (size_t)tenant * N * KW;
 
     // ---- staging assignment: per instruction i a wave moves rows
     //      32i + 8wv + (lane >> 3), lane l landing at LDS slot l & 7 ----
@@ -287,7 +451,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int r = 32 * i + 8 * wv + (lane >> 3);
-        const uint32_t xr = (uint32_t)min(m0 + r, M - 1);
+        // rows past the end (or past the tenant's last row) re-read a valid row
+        uint32_t xr;
+        if constexpr (GROUPED) xr = (uint32_t)(sRows[r] >= 0 ? sRows[r] : sRows[0]);
+        else xr = (uint32_t)min(m0 + r, M - 1);
         const uint32_t wr = (uint32_t)min(n0 + r, N - 1);
         xoff[i] = (xr * (uint32_t)K + 8u * ch) * 2u;
         woff[i] = (wr * (uint32_t)K + 8u * ch) * 2u;
@@ -469,7 +636,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     // ---- epilogue.  The W fragment is the MFMA's first operand, so acc[i][j][r]
     //      holds y[mrow + 32i][ncol + 32j + 8(r >> 2) + (r & 3)]: four
     //      consecutive columns per register quad ----
-    const int mrow = m0 + wm * 128 + (lane & 31);
+    const int lrow = wm * 128 + (lane & 31);
     const int ncol = n0 + wn * 128 + 4 * (lane >> 5);
     if constexpr (YDT == kBF16 && ALIGNED) {
         // Rows go through LDS, 64 at a time, so that each lane stores 16
@@ -499,8 +666,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
             for (int t = 0; t < 16; ++t) {
                 const int qd = lane + 64 * t, row = qd >> 4, c8 = qd & 15;
                 const u32x4 v = *reinterpret_cast<const u32x4*>(stage + row * kStageRow + c8 * 8);
-                const int gm = m0 + wm * 128 + 64 * half + row, gn = n0 + wn * 128 + c8 * 8;
-                if (gm < M && gn < N)
+                int gm;
+                const bool ok = out_row(wm * 128 + 64 * half + row, gm);
+                const int gn = n0 + wn * 128 + c8 * 8;
+                if (ok && gn < N)
                     *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(y) + (size_t)gm * N + gn) = v;
             }
         }
@@ -512,8 +681,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const int row = mrow + 32 * i, col = ncol + 32 * j + 8 * q;
-                    if (row >= M) continue;
+                    int row;
+                    if (!out_row(lrow + 32 * i, row)) continue;
+                    const int col = ncol + 32 * j + 8 * q;
                     float* dst = reinterpret_cast<float*>(y) + (size_t)row * N + col;
                     if constexpr (vec) {
                         if (col >= N) continue;
@@ -534,8 +704,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int row = mrow + 32 * i, col = ncol + 32 * j + 8 * (r >> 2) + (r & 3);
-                    if (row < M && col < N)
+                    int row;
+                    const bool ok = out_row(lrow + 32 * i, row);
+                    const int col = ncol + 32 * j + 8 * (r >> 2) + (r & 3);
+                    if (ok && col < N)
                         reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
                 }
     }
@@ -543,27 +715,66 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
 
 }  // namespace
 
+// The streaming kernel addresses x and W through buffer resources whose byte
+// extents must fit in 31 bits, and steps K in tiles of 64.
+bool prefill_stream_supported(int M, int N, int K) {
+    return K >= BK && K % BK == 0 && (int64_t)M * K < ((int64_t)1 << 30) &&
+           (int64_t)N * K < ((int64_t)1 << 30);
+}
+
 hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                           const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                           hipStream_t stream) {
     const int tiles_m = (M + BM - 1) / BM;
     const int tiles_n = (N + BN - 1) / BN;
-    // the streaming kernel addresses x and W through buffer resources whose
-    // byte extents must fit in 31 bits
-    const bool stream_ok = K >= BK && K % BK == 0 && (int64_t)M * K < ((int64_t)1 << 30) &&
-                           (int64_t)N * K < ((int64_t)1 << 30);
     const dim3 grid(tiles_m * tiles_n), block(kThreads);
-    if (stream_ok && y_dtype == kBF16 && N % 8 == 0)
-        prefill_stream_kernel<kBF16, true><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
-    else if (stream_ok && y_dtype == kBF16)
-        prefill_stream_kernel<kBF16, false><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
-    else if (stream_ok && N % 4 == 0)
-        prefill_stream_kernel<kF32, true><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
-    else if (stream_ok)
-        prefill_stream_kernel<kF32, false><<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, tiles_m, tiles_n);
+    const int32_t* no_ids = nullptr;
+    if (prefill_stream_supported(M, N, K)) {
+        if (y_dtype == kBF16 && N % 8 == 0)
+            prefill_stream_kernel<kBF16, true, false><<<grid, block, 0, stream>>>(
+                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+        else if (y_dtype == kBF16)
+            prefill_stream_kernel<kBF16, false, false><<<grid, block, 0, stream>>>(
+                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+        else if (N % 4 == 0)
+            prefill_stream_kernel<kF32, true, false><<<grid, block, 0, stream>>>(
+                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+        else
+            prefill_stream_kernel<kF32, false, false><<<grid, block, 0, stream>>>(
+                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+    } else {
+        prefill_general_kernel<<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype,
+                                                         tiles_m, tiles_n);
+    }
+    return hipGetLastError();
+}
+
+bool prefill_grouped_supported(int M, int N, int K, int T) {
+    return prefill_stream_supported(M, N, K) && T >= 1 && T <= kMaxGroupedTenants;
+}
+
+hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                                  const uint32_t* packed, const float* alpha,
+                                  const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                                  hipStream_t stream) {
+    // sum_t ceil(c_t / BM) over the U <= min(T, M) tenants present, with
+    // sum_t c_t <= M, is at most (M + (BM - 1) * U) / BM
+    const int64_t U = T < M ? T : M;
+    const int tiles_m = (int)(((int64_t)M + (BM - 1) * U) / BM);
+    const int tiles_n = (N + BN - 1) / BN;
+    const dim3 grid((tiles_m + 1) * tiles_n), block(kThreads);
+    if (y_dtype == kBF16 && N % 8 == 0)
+        prefill_stream_kernel<kBF16, true, true><<<grid, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
+    else if (y_dtype == kBF16)
+        prefill_stream_kernel<kBF16, false, true><<<grid, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
+    else if (N % 4 == 0)
+        prefill_stream_kernel<kF32, true, true><<<grid, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
     else
-        prefill_general_kernel<<<tiles_m * tiles_n, kThreads, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, y, y_dtype, tiles_m, tiles_n);
+        prefill_stream_kernel<kF32, false, true><<<grid, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
     return hipGetLastError();
 }
 

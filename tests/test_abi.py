@@ -92,7 +92,9 @@ def test_matmul_dtype_and_path_errors(lib):
     assert mm(lib, yd=bd.I8) == -4
     assert mm(lib, yd=7) == -4
     assert mm(lib, path=9) == -5
-    assert mm(lib, tid=0x60000000, path=bd.PATH_PREFILL) == -5
+    # the grouped fused GEMM needs K a multiple of 64 and at most 2048 tenants
+    assert mm(lib, K=96, tid=0x60000000, path=bd.PATH_PREFILL) == -5
+    assert mm(lib, T=2049, tid=0x60000000, path=bd.PATH_PREFILL) == -5
 
 
 def test_matmul_alias_errors(lib):
@@ -136,4 +138,8 @@ def test_path_selection(lib):
     assert bd.matmul_path(65, 4096, 4096, 1, False) == bd.PATH_PREFILL
     assert bd.matmul_path(4096, 4096, 4096, 1, False) == bd.PATH_PREFILL
     assert bd.matmul_path(32, 11008, 4096, 16, True) == bd.PATH_SKINNY
-    assert bd.matmul_path(4096, 4096, 4096, 8, True) == bd.PATH_SKINNY
+    assert bd.matmul_path(255, 4096, 4096, 8, True) == bd.PATH_SKINNY
+    assert bd.matmul_path(256, 4096, 4096, 8, True) == bd.PATH_PREFILL
+    assert bd.matmul_path(4096, 4096, 4096, 8, True) == bd.PATH_PREFILL
+    assert bd.matmul_path(4096, 4096, 4000, 8, True) == bd.PATH_SKINNY   # K % 64
+    assert bd.matmul_path(4096, 4096, 4096, 2049, True) == bd.PATH_SKINNY

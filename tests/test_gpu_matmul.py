@@ -342,3 +342,128 @@ def test_all_rows_one_tenant_matches_single_path():
     y = host_out(run_matmul(p))
     s = wl.Problem("t2", p.x, p.w, p.alpha[2:3], packed=p.packed[2:3], y_dtype="f32")
     np.testing.assert_allclose(y, host_out(run_matmul(s)), rtol=1e-6, atol=1e-6)
+
+
+# ------------------------------------------- batched form: grouped fused GEMM
+
+def _grouped(p, yd=None):
+    return host_out(run_matmul(p, path=PREFILL, y_dtype=yd))
+
+
+@pytest.mark.parametrize("M,N,K,T", [(65, 300, 128, 3), (300, 520, 576, 8), (513, 1000, 128, 17),
+                                     (1000, 257, 256, 2), (257, 255, 64, 5), (700, 70, 640, 40),
+                                     (2048, 300, 128, 1), (600, 513, 1088, 300)])
+@pytest.mark.parametrize("yd", ["f32", "bf16"])
+def test_grouped_prefill_ragged(M, N, K, T, yd):
+    p = wl.make_problem(M, N, K, T, seed=M + 3 * N + K + T, multi_tenant=True, y_dtype=yd)
+    log(f"grouped prefill M={M} N={N} K={K} T={T} {yd} present={len(np.unique(p.tenant_ids))}")
+    y = _grouped(p)
+    check(y, oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+
+
+@pytest.mark.parametrize("ids", ["prompts", "sorted", "one-of-eight", "big-tenant"])
+def test_grouped_prefill_equals_single_tenant_runs(ids):
+    # every row of tenant t gets exactly what the single-tenant fused kernel
+    # gives for that row with (alpha_t, S_t): same arithmetic, bit for bit
+    M, N, K, T = 900, 520, 256, 8
+    p = wl.make_problem(M, N, K, T, seed=21, multi_tenant=True, y_dtype="bf16")
+    rng = np.random.default_rng(22)
+    if ids == "prompts":
+        p.tenant_ids = wl.prompt_tenant_ids(rng, M, T, 6)
+    elif ids == "sorted":
+        p.tenant_ids = np.sort(p.tenant_ids)
+    elif ids == "one-of-eight":
+        p.tenant_ids = np.full(M, 5, np.int32)
+    else:
+        p.tenant_ids = np.where(rng.random(M) < 0.9, 2, rng.integers(0, T, M)).astype(np.int32)
+    log(f"grouped == per-tenant single runs, ids={ids}")
+    y = run_matmul(p, path=PREFILL)
+    t = torch()
+    for ten in np.unique(p.tenant_ids):
+        rows = np.nonzero(p.tenant_ids == ten)[0]
+        q = wl.Problem("one", p.x[rows], p.w, p.alpha[ten:ten + 1], packed=p.packed[ten:ten + 1],
+                       y_dtype="bf16")
+        ys = run_matmul(q, path=PREFILL)
+        assert t.equal(y[t.from_numpy(rows).cuda()].view(t.int16), ys.view(t.int16)), ten
+
+
+def test_grouped_prefill_invalid_ids_nan_rows():
+    M, N, K, T = 400, 300, 192, 4
+    p = wl.make_problem(M, N, K, T, seed=23, multi_tenant=True, y_dtype="f32")
+    log("grouped prefill invalid ids")
+    y = _grouped(p)
+    bad = p.tenant_ids.copy()
+    idx = [0, 1, 255, 256, 399]
+    bad[idx] = [-1, T, 1 << 30, -(1 << 31), T + 7]
+    r = wl.Problem("bad", p.x, p.w, p.alpha, packed=p.packed, tenant_ids=bad, y_dtype="f32")
+    yb = _grouped(r)
+    assert np.all(np.isnan(yb[idx]))
+    keep = np.setdiff1d(np.arange(M), idx)
+    np.testing.assert_array_equal(yb[keep], y[keep])
+    # every id invalid: all rows NaN
+    r.tenant_ids = np.full(M, -3, np.int32)
+    assert np.all(np.isnan(_grouped(r)))
+
+
+@pytest.mark.parametrize("T", [1, 3])
+def test_grouped_prefill_effective_weight_exact(T):
+    # one-hot rows spread over the tenants: y[row, n] = bf16_rne(W[n,k] + s_t[n,k] alpha_t)
+    K, N = 384, 264
+    base = wl.make_problem(1, N, K, T, seed=24)
+    cols = np.arange(K)
+    rows = np.concatenate([cols] * 2)  # 768 rows: several tiles per tenant
+    x = np.zeros((len(rows), K), np.uint16)
+    x[np.arange(len(rows)), rows] = 0x3F80
+    tid = np.random.default_rng(25).integers(0, T, len(rows)).astype(np.int32)
+    p = wl.Problem("onehot-grouped", x, base.w, base.alpha, packed=base.packed, tenant_ids=tid,
+                   y_dtype="f32")
+    log(f"grouped effective-weight rounding T={T}")
+    y = _grouped(p)
+    ref = np.empty_like(y)
+    wv = wl.bf16_bits_to_f32(p.w)
+    for ten in range(T):
+        s = oracle.unpack(p.packed[ten], K)  # [N, K]
+        a = np.float32(p.alpha[ten])
+        eff = (wv + np.where(s > 0, a, -a).astype(np.float32)).astype(np.float32)
+        effb = wl.bf16_bits_to_f32(wl.f32_to_bf16_bits(eff))  # [N, K]
+        sel = np.nonzero(tid == ten)[0]
+        ref[sel] = effb[:, rows[sel]].T
+    assert np.array_equal(y, ref)
+
+
+def test_grouped_prefill_tenant_limit():
+    import paper_2609_36800_amd as bd
+    M, N, K = 300, 64, 128
+    p = wl.make_problem(M, N, K, 2048, seed=26, multi_tenant=True, y_dtype="f32")
+    log("grouped prefill T=2048 (limit)")
+    check(_grouped(p), oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    assert bd.matmul_path(M, N, K, 2048, True) == PREFILL
+    assert bd.matmul_path(M, N, K, 2049, True) == SKINNY
+
+
+def test_grouped_prefill_deterministic():
+    p = wl.make_problem(700, 600, 512, 6, seed=27, multi_tenant=True)
+    log("grouped prefill determinism")
+    t = torch()
+    y1 = run_matmul(p, path=PREFILL)
+    y2 = run_matmul(p, path=PREFILL)
+    assert t.equal(y1.view(t.int16), y2.view(t.int16))
+
+
+def test_mt_prefill_workload_sampled():
+    p = wl.mt_prefill(seed=0)
+    log(f"multi-tenant prefill workload: {p.name}, tenants present {len(np.unique(p.tenant_ids))}")
+    import paper_2609_36800_amd as bd
+    assert bd.matmul_path(p.M, p.N, p.K, p.T, True) == PREFILL
+    y = run_matmul(p)
+    rng = np.random.default_rng(2)
+    # sampled rows include each tenant's first and last row (tile edges of the grouping)
+    edges = []
+    for ten in np.unique(p.tenant_ids):
+        r = np.nonzero(p.tenant_ids == ten)[0]
+        edges += [r[0], r[-1], r[min(len(r) - 1, 255)], r[min(len(r) - 1, 256)]]
+    rows = np.unique(np.concatenate([sample_cols(p.M, 192, rng), np.array(edges)]))
+    cols = sample_cols(p.N, 192, rng)
+    yh = host_out(y[rows][:, cols])
+    ref = oracle_y(p, rows=rows, cols=cols)
+    check(yh, ref, p.x, p.w, p.alpha, p.tenant_ids[rows], rows=rows)

@@ -12,6 +12,8 @@ workloads below are LLaMA-7B-shaped stand-ins:
   decode       x {1,16}x4096, W 4096x4096, one tenant, bf16 output
   mt_decode    x 32x4096, W 11008x4096, 16 tenants, per-row tenant id, bf16 output
   prefill      x 4096x4096, W 4096x4096, one tenant, bf16 output
+  mt_prefill   x 4096x4096 as 16 prompts of random length, one tenant per
+               prompt drawn from 8, W 4096x4096, bf16 output
   llama_sweep  32 layers x {q,k,v,o 4096x4096; gate,up 11008x4096;
                down 4096x11008}, 8 tenants, 64 token rows, bf16 output
 
@@ -108,6 +110,16 @@ def tenant_draw(rng: np.random.Generator, M: int, T: int) -> np.ndarray:
     return rng.integers(0, T, size=M, dtype=np.int64).astype(np.int32)
 
 
+def prompt_tenant_ids(rng: np.random.Generator, M: int, T: int, prompts: int) -> np.ndarray:
+    """Tenant id per row for M token rows that come as `prompts` consecutive
+    prompts: lengths from prompts-1 distinct cut points drawn uniformly in
+    (0, M), each prompt's tenant uniform over [0, T)."""
+    cuts = np.sort(rng.choice(np.arange(1, M), size=prompts - 1, replace=False))
+    lengths = np.diff(np.concatenate([[0], cuts, [M]]))
+    tenants = rng.integers(0, T, size=prompts, dtype=np.int64)
+    return np.repeat(tenants, lengths).astype(np.int32)
+
+
 def make_problem(M: int, N: int, K: int, T: int = 1, *, seed: int = 0,
                  multi_tenant: bool = False, y_dtype: str = "bf16",
                  x_std: float = 1.0, w_std: float = 0.02,
@@ -145,6 +157,17 @@ def prefill(seed: int = 0) -> Problem:
     return make_problem(4096, 4096, 4096, 1, seed=seed, name="prefill 4096^3")
 
 
+MT_PREFILL = {"M": 4096, "N": 4096, "K": 4096, "T": 8, "prompts": 16}
+
+
+def mt_prefill(seed: int = 0) -> Problem:
+    c = MT_PREFILL
+    p = make_problem(c["M"], c["N"], c["K"], c["T"], seed=seed,
+                     name="multi-tenant prefill 4096 rows (16 prompts, 8 tenants) x 4096x4096")
+    p.tenant_ids = prompt_tenant_ids(np.random.default_rng([seed, 3]), c["M"], c["T"], c["prompts"])
+    return p
+
+
 def llama_shared_inputs(seed: int = 0):
     """x for K=4096 and K=11008 (64 rows each) and the 64 tenant ids."""
     rng = np.random.default_rng([seed, 1])
@@ -177,11 +200,12 @@ def llama_matrix(layer: int, idx: int, shared=None, seed: int = 0) -> Problem:
 # ---- device-side generation for the benchmark (same recipe, torch RNG) ----
 
 def device_problem(M: int, N: int, K: int, T: int, *, multi_tenant: bool, seed: int,
-                   device="cuda", x_std: float = 1.0, w_std: float = 0.02):
+                   device="cuda", x_std: float = 1.0, w_std: float = 0.02, prompts: int = 0):
     """Same distributions, drawn directly into device memory with torch's RNG.
 
     Returns a dict of torch tensors: x (bf16 [M,K]), w (bf16 [N,K]),
     packed (int32 [T,N,K/32]), alpha (fp32 [T]), tenant_ids (int32 [M] or None).
+    With prompts > 0 the tenant ids follow prompt_tenant_ids (drawn on the host).
     """
     import torch
     g = torch.Generator(device=device)
@@ -195,6 +219,9 @@ def device_problem(M: int, N: int, K: int, T: int, *, multi_tenant: bool, seed: 
     alpha = (torch.rand((T,), generator=g, device=device, dtype=torch.float32)
              * 9e-4 + 1e-4)
     tid = None
-    if multi_tenant:
+    if multi_tenant and prompts > 0:
+        ids = prompt_tenant_ids(np.random.default_rng([seed, 3]), M, T, prompts)
+        tid = torch.from_numpy(ids).to(device)
+    elif multi_tenant:
         tid = torch.randint(0, T, (M,), generator=g, device=device, dtype=torch.int32)
     return {"x": x, "w": w, "packed": packed, "alpha": alpha, "tenant_ids": tid}
