@@ -57,7 +57,7 @@ typedef enum {
 typedef enum {
     BITDELTA_PATH_AUTO = 0,
     BITDELTA_PATH_SKINNY = 1,   /* M <= 64, any tenants: HBM-bound decode path   */
-    BITDELTA_PATH_PREFILL = 2   /* one tenant, any M: fused (W + alpha*s) GEMM   */
+    BITDELTA_PATH_PREFILL = 2   /* fused (W + alpha_t*s_t) GEMM per tenant      */
 } bitdelta_path;
 
 /*
@@ -99,13 +99,16 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K,
  *               overlap any input
  *
  * Accumulation is fp32; a bf16 output is rounded to nearest-even once at the
- * end.  The single-tenant path for M > 64 rounds the effective weight
- * W_base + alpha*s to bf16 before its one matrix-core GEMM; the M <= 64 path
- * keeps the two sums apart and never rounds the weight.
+ * end.  The fused path (single tenant with M > 64, batched with M >= 256)
+ * rounds the effective weight W_base + alpha_t*s_t to bf16 before its one
+ * matrix-core GEMM; the decode-shaped path keeps the two sums apart and
+ * never rounds the weight.
  * A row whose tenant id is outside [0, T) is written as quiet NaN (ids live in
  * device memory, so they are not checked on the host).
  * M == 0 or N == 0 is a no-op; K == 0 writes zeros.
- * Multi-tenant requests with M > 64 are served 64 rows at a time.
+ * Batched requests with M >= 256, K a multiple of 64 and T <= 2048 run one
+ * fused GEMM per tenant over that tenant's rows (grouped on the device);
+ * other batched requests with M > 64 are served 64 rows at a time.
  * Errors: NULL, SHAPE, ALIGN, DTYPE, ALIAS, HIP.
  */
 int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K,
@@ -117,8 +120,9 @@ int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K,
 /*
  * Same as bitdelta_matmul with the kernel path chosen by the caller (tests
  * exercise each path on the same inputs).  BITDELTA_PATH_PREFILL with
- * tenant_ids != NULL returns BITDELTA_ERR_UNSUPPORTED; BITDELTA_PATH_SKINNY
- * accepts any M (64 rows per launch).
+ * tenant_ids != NULL needs K a multiple of 64, T <= 2048 and M*K, N*K below
+ * 2^30, else it returns BITDELTA_ERR_UNSUPPORTED; BITDELTA_PATH_SKINNY accepts
+ * any M (64 rows per launch).
  */
 int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K,
                               const uint16_t* w_base, int64_t N,
