@@ -12,6 +12,9 @@ Appendix A.2, "BitDelta" paragraph):
 
     y[m, n] = sum_k x[m, k] W[n, k] + alpha[t(m)] * sum_k x[m, k] s_t(m)[n, k]
 
+It also holds the compression of a fine-tuned weight into that form
+(``compress``: the signs of W_fine - W_base and their least-squares scale).
+
 Every function here is pinned by ``tests/test_oracle.py`` against facts that do
 not come from the oracle itself (library packers, exact brute force, closed
 forms, algebraic identities).
@@ -62,6 +65,8 @@ def _load():
         f.restype = ctypes.c_int
     lib.oracle_unpack_f64.argtypes = [P, I64, I64, P]
     lib.oracle_unpack_f64.restype = ctypes.c_int
+    lib.oracle_compress.argtypes = [P, P, I64, I64, P, P, P]
+    lib.oracle_compress.restype = ctypes.c_int
     lib.oracle_matmul_parts.argtypes = [P, I64, I64, P, I64, P, P, P, ctypes.c_int32,
                                         P, I64, P, P, P]
     lib.oracle_matmul_parts.restype = ctypes.c_int
@@ -113,6 +118,33 @@ def unpack(packed: np.ndarray, K: int) -> np.ndarray:
     if rc != 0:
         raise RuntimeError(f"oracle unpack failed ({rc})")
     return out
+
+
+def compress(fine_bits, base_bits):
+    """Binary delta of a fine-tuned weight against its base, in fp64.
+
+    fine_bits, base_bits  uint16 [rows, K] (bf16 bit patterns)
+    Returns (packed uint32 [rows, K/32], row_abs float64 [rows], alpha float):
+    the packed signs of delta = fine - base (bit set when delta's sign bit is
+    clear), sum_k |delta| per row, and alpha = mean |delta|, the scale that
+    minimises ||delta - alpha * s||_F for those signs.
+    """
+    lib = _load()
+    fine_bits = np.ascontiguousarray(fine_bits, dtype=np.uint16)
+    base_bits = np.ascontiguousarray(base_bits, dtype=np.uint16)
+    if fine_bits.shape != base_bits.shape or fine_bits.ndim != 2:
+        raise ValueError("fine and base must be [rows, K] of the same shape")
+    rows, K = fine_bits.shape
+    if K % 32:
+        raise ValueError("K must be a multiple of 32")
+    packed = np.zeros((rows, K // 32), dtype=np.uint32)
+    row_abs = np.zeros(rows, dtype=np.float64)
+    alpha = np.zeros(1, dtype=np.float64)
+    rc = lib.oracle_compress(_ptr(fine_bits), _ptr(base_bits), rows, K, _ptr(packed),
+                             _ptr(row_abs), _ptr(alpha))
+    if rc != 0:
+        raise RuntimeError(f"oracle compress failed ({rc})")
+    return packed, row_abs, float(alpha[0])
 
 
 def matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None):

@@ -14,6 +14,8 @@
  *                 axis and bit order are this library's stated format.
  *   pack          bit = 1 exactly when the input's IEEE / two's-complement
  *                 sign bit is clear (so +1 -> 1, -1 -> 0).
+ *   compress      delta = W_fine - W_base; packed = pack(delta); the scale is
+ *                 the mean of |delta| (the least-squares scale for the signs).
  *   matmul        y[m][n] = sum_k x[m][k] W[n][k]
  *                         + alpha[t] * sum_k x[m][k] s_t[n][k],  t = tenant(m)
  *                 i.e. the standard (single-tenant) and batched (per-row
@@ -120,6 +122,43 @@ int oracle_unpack_f64(const uint32_t* packed, int64_t rows, int64_t K, double* o
     for (int64_t r = 0; r < rows; ++r)
         for (int64_t k = 0; k < K; ++k)
             out[r * K + k] = sign_at(packed + r * words, k);
+    return 0;
+}
+
+/* ---- compress: sign of the delta and its least-squares scale ------------
+ *
+ *   delta[n][k] = W_fine[n][k] - W_base[n][k]   (fp64; exact unless the two
+ *                 exponents differ by more than 45, and its sign always is)
+ *   packed      = the pack rule applied to delta (bit set when delta's sign
+ *                 bit is clear, so delta = +0 gives +1)
+ *   row_abs[n]  = sum_k |delta[n][k]|           (k ascending)
+ *   alpha       = sum_n row_abs[n] / (rows * K)
+ *
+ * With the sign matrix s fixed to the signs of delta, the scale a minimising
+ * sum (delta - a s)^2 makes the derivative -2 sum s (delta - a s) vanish;
+ * s*s = 1 and s*delta = |delta| turn that into a = sum |delta| / (rows * K).
+ * The binary delta the paper's kernel decodes (Appendix A.2) is this pair.
+ */
+int oracle_compress(const uint16_t* fine, const uint16_t* base, int64_t rows, int64_t K,
+                    uint32_t* packed, double* row_abs, double* alpha) {
+    if (K % 32 != 0 || rows < 0 || K < 0) return -2;
+    int64_t n = rows * K;
+    uint8_t* sb = (uint8_t*)malloc((size_t)(n > 0 ? n : 1));
+    if (!sb) return -7;
+    double total = 0.0;
+    for (int64_t r = 0; r < rows; ++r) {
+        double acc = 0.0;
+        for (int64_t k = 0; k < K; ++k) {
+            double d = bf16_to_double(fine[r * K + k]) - bf16_to_double(base[r * K + k]);
+            sb[r * K + k] = (uint8_t)(signbit(d) ? 1 : 0);
+            acc += fabs(d);
+        }
+        if (row_abs) row_abs[r] = acc;
+        total += acc;
+    }
+    pack_bits(sb, rows, K, packed);
+    free(sb);
+    if (alpha) *alpha = n > 0 ? total / (double)n : 0.0;
     return 0;
 }
 

@@ -267,3 +267,97 @@ def test_empty_shapes():
     y = oracle.matmul(np.zeros((2, 0), np.uint16), np.zeros((3, 0), np.uint16),
                       np.zeros((1, 3, 0), np.uint32), np.ones(1, np.float32))
     assert np.array_equal(y, np.zeros((2, 3)))
+
+
+# ---------------------------------------------------------------- compress
+
+def _fraction_bf16(bits):
+    from fractions import Fraction
+    return Fraction(float(wl.bf16_bits_to_f32(np.array([bits], np.uint16))[0]))
+
+
+def test_compress_bits_equal_numpy_signbit():
+    # library routine: numpy's fp64 difference, np.signbit and packbits
+    rng = np.random.default_rng(30)
+    for rows, K in ((3, 32), (17, 96), (64, 1024)):
+        base = wl.normal_bf16(rng, (rows, K), 0.02)
+        fine = wl.normal_bf16(rng, (rows, K), 0.02)
+        fine[:, ::7] = base[:, ::7]  # equal entries: delta = +0 -> +1
+        packed, _, _ = oracle.compress(fine, base)
+        d = bf16(fine) - bf16(base)
+        np.testing.assert_array_equal(packed, numpy_pack(~np.signbit(d)))
+
+
+def test_compress_sums_exact_brute_force():
+    # exact rational sums of |fine - base| (bf16 values are dyadic rationals)
+    from fractions import Fraction
+    rng = np.random.default_rng(31)
+    rows, K = 3, 64
+    base = wl.normal_bf16(rng, (rows, K), 1.0)
+    fine = wl.normal_bf16(rng, (rows, K), 1e-3)  # very different magnitudes
+    _, row_abs, alpha = oracle.compress(fine, base)
+    exact = [sum((abs(_fraction_bf16(fine[r, k]) - _fraction_bf16(base[r, k])) for k in range(K)),
+                 Fraction(0)) for r in range(rows)]
+    for r in range(rows):
+        assert abs(Fraction(row_abs[r]) - exact[r]) <= exact[r] * Fraction(1, 10 ** 14)
+    mean = sum(exact, Fraction(0)) / (rows * K)
+    assert abs(Fraction(alpha) - mean) <= mean * Fraction(1, 10 ** 14)
+
+
+def test_compress_closed_form_scaled_signs():
+    # base = 0, fine = c * s with c = 2^-7 (exact in bf16): signs come back, alpha = c
+    rng = np.random.default_rng(32)
+    rows, K = 9, 160
+    s = np.where(rng.random((rows, K)) < 0.5, 1.0, -1.0).astype(np.float32)
+    c = 2.0 ** -7
+    fine = wl.f32_to_bf16_bits(s * np.float32(c))
+    base = np.zeros((rows, K), np.uint16)
+    packed, row_abs, alpha = oracle.compress(fine, base)
+    np.testing.assert_array_equal(packed, numpy_pack(s > 0))
+    assert alpha == c
+    assert np.all(row_abs == K * c)
+
+
+def test_compress_least_squares_scale():
+    # alpha minimises ||delta - a*s||^2 for the returned signs: the derivative
+    # sum s (delta - alpha s) vanishes and nearby scales do worse
+    rng = np.random.default_rng(33)
+    rows, K = 40, 512
+    base = wl.normal_bf16(rng, (rows, K), 0.02)
+    fine = wl.f32_to_bf16_bits(bf16(base).astype(np.float32)
+                               + rng.standard_normal((rows, K)).astype(np.float32) * 1e-3)
+    packed, _, alpha = oracle.compress(fine, base)
+    d = bf16(fine) - bf16(base)
+    s = numpy_signs(packed, K)
+
+    def obj(a):
+        return float(np.sum((d - a * s) ** 2))
+    grad = float(np.sum(s * (d - alpha * s)))
+    assert abs(grad) <= 1e-9 * float(np.sum(np.abs(d)))
+    assert obj(alpha) < obj(alpha * (1 + 1e-3)) and obj(alpha) < obj(alpha * (1 - 1e-3))
+
+
+def test_compress_worked_rows_and_signed_zeros():
+    # hand-derived words: bit i of word 0 <-> k = i; +1 where fine - base >= +0
+    K = 32
+    half, quarter = 0x3F00, 0x3E80          # 0.5, 0.25 in bf16
+    one, one5, two = 0x3F80, 0x3FC0, 0x4000  # 1.0, 1.5, 2.0
+    base = np.full((4, K), half, np.uint16)
+    fine = base.copy()
+    # row 0: +0.25 at even k, -0.25 at odd k  -> 0x55555555, |delta| = 0.25 each
+    fine[0, 0::2] = 0x3F40                   # 0.75
+    fine[0, 1::2] = quarter
+    # row 1: equal -> delta = +0 everywhere -> 0xFFFFFFFF, sum 0
+    # row 2: 1.0 - 1.5 = -0.5 everywhere except k = 31 where 2.0 - 1.5 = +0.5 -> 0x80000000
+    base[2] = one5
+    fine[2] = one
+    fine[2, 31] = two
+    # row 3: signed zeros: (-0) - (+0) = -0 -> 0 at k=0; (+0) - (-0) = +0 -> 1 at k=1;
+    #        (-0) - (-0) = +0 -> 1 at k=2; the rest equal -> 1
+    base[3, 0], fine[3, 0] = 0x0000, 0x8000
+    base[3, 1], fine[3, 1] = 0x8000, 0x0000
+    base[3, 2], fine[3, 2] = 0x8000, 0x8000
+    packed, row_abs, alpha = oracle.compress(fine, base)
+    assert [int(w) for w in packed[:, 0]] == [0x55555555, 0xFFFFFFFF, 0x80000000, 0xFFFFFFFE]
+    assert list(row_abs) == [8.0, 0.0, 16.0, 0.0]
+    assert alpha == 24.0 / (4 * K)
