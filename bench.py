@@ -209,6 +209,50 @@ def llama_sweep(dev, launcher, warmup):
             "TBps": total_bytes / secs / 1e12, "per_matrix": per_matrix}
 
 
+def bench_compress(dev, lib, steps, warmup):
+    """Delta compression of LLaMA-7B-gate-shaped weights (11008x4096 bf16 fine and
+    base -> packed signs, per-row |delta| sums, scale), buffer sets rotating over
+    more than twice the Infinity Cache.  HBM-bound: 4 bytes read per weight."""
+    import ctypes
+    import torch
+    rows, K = 11008, 4096
+    per = rows * K * 4 + rows * K // 8 + rows * 4 + 4
+    nsets = max(2, -(-2 * MALL_BYTES // per))
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    sets = []
+    for _ in range(nsets):
+        base = (torch.randn((rows, K), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+        fine = (base.float() + torch.randn((rows, K), generator=g, device=dev) * 1e-3).to(torch.bfloat16)
+        packed = torch.empty((rows, K // 32), dtype=torch.int32, device=dev)
+        row_abs = torch.empty((rows,), dtype=torch.float32, device=dev)
+        alpha = torch.empty((1,), dtype=torch.float32, device=dev)
+        sets.append((fine, base, packed, row_abs, alpha))
+    f = lib.bitdelta_compress
+
+    def call_for(st):
+        fine, base, packed, row_abs, alpha = st
+        args = (fine.data_ptr(), base.data_ptr(), rows, K, packed.data_ptr(), row_abs.data_ptr(),
+                alpha.data_ptr())
+
+        def c():
+            rc = f(*args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"bitdelta_compress failed: {rc}")
+        return c
+    calls = [call_for(sets[i % nsets]) for i in range(steps)]
+    warm = [call_for(sets[i % nsets]) for i in range(max(1, warmup))]
+    replay, graphed, graph = capture(calls, warm)
+    secs = timed(replay, 1)
+    del graph, sets
+    torch.cuda.empty_cache()
+    return {"workload": "delta compression: W_fine, W_base 11008x4096 bf16 -> packed signs, "
+                        "per-row |delta| sums and the least-squares scale",
+            "steps": steps, "graphed": graphed, "buffer_sets": nsets,
+            "us_per_call": secs / steps * 1e6, "bytes_per_call": per,
+            "TBps": per * steps / secs / 1e12}
+
+
 def cpu_baseline(budget_s: float):
     """fp64 oracle timed on the headline workload (the M = 1 and M = 16 pair
     against one 4096x4096 matrix), repeated until about budget_s seconds."""
@@ -411,6 +455,7 @@ def main():
         mpf["mfma_frac"] = mpf["TFLOPs"] / BF16_PEAK_TFLOPS
         workloads.append(mpf)
         workloads.append(llama_sweep(dev, launcher, args.warmup))
+        workloads.append(bench_compress(dev, launcher.lib, 50, args.warmup))
 
     cpu = None if args.no_cpu else cpu_baseline(args.cpu_budget)
 

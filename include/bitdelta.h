@@ -86,6 +86,34 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K,
                     void* signs, int out_dtype, hipStream_t stream);
 
 /*
+ * Compress a fine-tuned weight against its base into the binary-delta form
+ * the matmul consumes (the packed signs of Appendix A.2 and one scale):
+ *
+ *   delta[n][k]     = w_fine[n][k] - w_base[n][k], computed in fp32 (its
+ *                     sign is always exact)
+ *   packed          bit set where delta's sign bit is clear (delta = +0
+ *                   gives +1), by the same rule as bitdelta_pack
+ *   row_abs_sum[n]  = sum_k |delta[n][k]| (fp32, fixed summation order)
+ *   alpha[0]        = sum_n row_abs_sum[n] / (rows * K), summed in fp64
+ *
+ * alpha is the least-squares scale for these signs: it minimises
+ * ||delta - a * s||_F over a (the derivative vanishes at a = mean |delta|).
+ *
+ *   w_fine, w_base  [rows][K] bf16, 16-byte aligned
+ *   packed          [rows][K/32] uint32 output, 4-byte aligned
+ *   row_abs_sum     [rows] fp32 output, 4-byte aligned (also holds the
+ *                   partial sums of the alpha reduction)
+ *   alpha           [1] fp32 output, or NULL to skip the mean
+ *
+ * Inputs are expected finite and free of bf16 subnormals.  rows == 0 or
+ * K == 0 is a no-op.  Outputs must not overlap inputs or each other.
+ * Errors: NULL, SHAPE (rows < 0, K < 0, K % 32), ALIGN, ALIAS, HIP.
+ */
+int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base,
+                      int64_t rows, int64_t K, uint32_t* packed,
+                      float* row_abs_sum, float* alpha, hipStream_t stream);
+
+/*
  * Binary-delta matmul, standard and batched (multi-tenant) forms (Section 4.4).
  *
  *   x           [M][K] bf16, 16-byte aligned

@@ -28,6 +28,7 @@ PATH_AUTO, PATH_SKINNY, PATH_PREFILL = 0, 1, 2
 EXPORTED = (
     "bitdelta_pack",
     "bitdelta_unpack",
+    "bitdelta_compress",
     "bitdelta_matmul",
     "bitdelta_matmul_with_path",
     "bitdelta_matmul_path",
@@ -59,6 +60,8 @@ def load_library(path: str = LIB_PATH):
     lib.bitdelta_pack.restype = I
     lib.bitdelta_unpack.argtypes = [P, I64, I64, P, I, P]
     lib.bitdelta_unpack.restype = I
+    lib.bitdelta_compress.argtypes = [P, P, I64, I64, P, P, P, P]
+    lib.bitdelta_compress.restype = I
     lib.bitdelta_matmul.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, P]
     lib.bitdelta_matmul.restype = I
     lib.bitdelta_matmul_with_path.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, I, P]
@@ -129,6 +132,28 @@ def unpack(packed, K: int, dtype=None, out=None):
     _check(load_library().bitdelta_unpack(packed.data_ptr(), rows, K, out.data_ptr(),
                                           _dtype_code(out.dtype), _stream(packed)))
     return out
+
+
+def compress(w_fine, w_base, with_alpha: bool = True):
+    """Binary delta of w_fine against w_base (both bf16 [rows, K]).
+
+    Returns (packed int32 [rows, K/32], alpha fp32 [1] or None, row_abs_sum
+    fp32 [rows]): the packed signs of w_fine - w_base, their least-squares
+    scale mean|w_fine - w_base|, and the per-row sums of |w_fine - w_base|.
+    """
+    import torch
+    _dev(w_fine, "w_fine", (torch.bfloat16,))
+    _dev(w_base, "w_base", (torch.bfloat16,))
+    if w_fine.shape != w_base.shape or w_fine.dim() != 2:
+        raise ValueError("w_fine and w_base must be [rows, K] of the same shape")
+    rows, K = w_fine.shape
+    packed = torch.empty((rows, K // 32), dtype=torch.int32, device=w_fine.device)
+    row_abs = torch.empty((rows,), dtype=torch.float32, device=w_fine.device)
+    alpha = torch.empty((1,), dtype=torch.float32, device=w_fine.device) if with_alpha else None
+    _check(load_library().bitdelta_compress(
+        w_fine.data_ptr(), w_base.data_ptr(), rows, K, packed.data_ptr(), row_abs.data_ptr(),
+        None if alpha is None else alpha.data_ptr(), _stream(w_fine)))
+    return packed, alpha, row_abs
 
 
 def matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=None, out=None,

@@ -113,6 +113,27 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K, void* signs
     return hip_status(bitdelta::launch_unpack(packed, rows * K, signs, out_dtype, stream));
 }
 
+int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base, int64_t rows, int64_t K,
+                      uint32_t* packed, float* row_abs_sum, float* alpha, hipStream_t stream) {
+    if (rows < 0 || K < 0 || K % 32 != 0 || rows > kMaxDim || K > kMaxDim) return BITDELTA_ERR_SHAPE;
+    if (rows == 0 || K == 0) return BITDELTA_OK;
+    if (w_fine == nullptr || w_base == nullptr || packed == nullptr || row_abs_sum == nullptr)
+        return BITDELTA_ERR_NULL;
+    if (!aligned(w_fine, 16) || !aligned(w_base, 16) || !aligned(packed, 4) ||
+        !aligned(row_abs_sum, 4) || !aligned(alpha, 4))
+        return BITDELTA_ERR_ALIGN;
+    const size_t wbytes = (size_t)rows * K * 2, pbytes = (size_t)rows * (K / 32) * 4,
+                 rbytes = (size_t)rows * 4, abytes = alpha ? 4 : 0;
+    if (overlaps(packed, pbytes, w_fine, wbytes) || overlaps(packed, pbytes, w_base, wbytes) ||
+        overlaps(row_abs_sum, rbytes, w_fine, wbytes) || overlaps(row_abs_sum, rbytes, w_base, wbytes) ||
+        overlaps(row_abs_sum, rbytes, packed, pbytes) || overlaps(alpha, abytes, w_fine, wbytes) ||
+        overlaps(alpha, abytes, w_base, wbytes) || overlaps(alpha, abytes, packed, pbytes) ||
+        overlaps(alpha, abytes, row_abs_sum, rbytes))
+        return BITDELTA_ERR_ALIAS;
+    return hip_status(bitdelta::launch_compress(w_fine, w_base, (int)rows, (int)K, packed,
+                                                row_abs_sum, alpha, stream));
+}
+
 int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
     return choose_path(M, N, K, T, has_tenant_ids);
 }

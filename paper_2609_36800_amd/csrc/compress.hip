@@ -1,0 +1,110 @@
+// Compression of a fine-tuned weight into the binary-delta form the matmul
+// kernels decode (packed signs, one scale; storage format of Appendix A.2):
+//
+//   delta[n][k] = W_fine[n][k] - W_base[n][k]                 (fp32)
+//   bit (n, k)  = 1 where delta's sign bit is clear, else 0    (same rule as pack)
+//   row_abs[n]  = sum_k |delta[n][k]|                          (fp32, fixed order)
+//   alpha       = sum_n row_abs[n] / (rows * K)                (fp64 sum, fp32 result)
+//
+// alpha is the least-squares scale for those signs: with s fixed, the a that
+// minimises sum (delta - a s)^2 satisfies sum s (delta - a s) = 0, and
+// s * s = 1, s * delta = |delta| give a = mean |delta|.
+//
+// The difference of two bf16 values has the exact sign in fp32 (a nonzero
+// difference is at least 2^-133 in magnitude, far above fp32's smallest
+// subnormal), and is exact itself unless the exponents differ by more than 15
+// (two 8-bit significands then span more than fp32's 24 bits).
+//
+// compress_kernel streams both weights once (HBM-bound: 4 bytes read per
+// element, 1/8 written): one wave per row, lane l taking 8 consecutive elements
+// of each 512-element chunk, so its 8 sign bits are byte l of the chunk's
+// packed words and a wave's byte stores cover 64 contiguous bytes.  Four
+// chunks are loaded before any is used.  The per-lane sums are added in a
+// fixed butterfly, so the result does not depend on scheduling.
+// mean_kernel (one workgroup) then reduces the per-row sums in a fixed order.
+#include "device.h"
+#include "internal.h"
+
+namespace bitdelta {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kChunk = 512;  // elements per wave-wide 16-byte load
+constexpr int kUnroll = 4;
+
+__device__ __forceinline__ float lo_f32(uint32_t v) { return __builtin_bit_cast(float, v << 16); }
+__device__ __forceinline__ float hi_f32(uint32_t v) { return __builtin_bit_cast(float, v & 0xFFFF0000u); }
+
+__global__ __launch_bounds__(kWaves * 64) void compress_kernel(
+    const uint16_t* __restrict__ fine, const uint16_t* __restrict__ base, int rows, int K,
+    uint32_t* __restrict__ packed, float* __restrict__ row_abs) {
+    const int lane = threadIdx.x & 63;
+    const int row = blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (row >= rows) return;  // whole waves leave; there is no barrier
+    const uint16_t* f = fine + (size_t)row * K;
+    const uint16_t* b = base + (size_t)row * K;
+    uint8_t* out = reinterpret_cast<uint8_t*>(packed + (size_t)row * (K / 32));
+
+    float acc = 0.f;
+    for (int k0 = 0; k0 < K; k0 += kChunk * kUnroll) {
+        u32x4 fv[kUnroll], bv[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int k = k0 + kChunk * u + 8 * lane;
+            if (k < K) {
+                fv[u] = load16(f + k);
+                bv[u] = load16(b + k);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int k = k0 + kChunk * u + 8 * lane;
+            if (k >= K) continue;
+            uint32_t byte = 0;
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const float dl = lo_f32(fv[u][p]) - lo_f32(bv[u][p]);
+                const float dh = hi_f32(fv[u][p]) - hi_f32(bv[u][p]);
+                byte |= ((~__builtin_bit_cast(uint32_t, dl)) >> 31) << (2 * p);
+                byte |= ((~__builtin_bit_cast(uint32_t, dh)) >> 31) << (2 * p + 1);
+                acc += __builtin_fabsf(dl);
+                acc += __builtin_fabsf(dh);
+            }
+            out[k >> 3] = (uint8_t)byte;
+        }
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d);
+    if (lane == 0) row_abs[row] = acc;
+}
+
+constexpr int kMeanThreads = 256;
+
+__global__ __launch_bounds__(kMeanThreads) void mean_kernel(const float* __restrict__ row_abs,
+                                                            int rows, double count,
+                                                            float* __restrict__ alpha) {
+    __shared__ double part[kMeanThreads];
+    double s = 0.0;
+    for (int i = threadIdx.x; i < rows; i += kMeanThreads) s += (double)row_abs[i];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int d = kMeanThreads / 2; d > 0; d >>= 1) {
+        if ((int)threadIdx.x < d) part[threadIdx.x] += part[threadIdx.x + d];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) alpha[0] = (float)(part[0] / count);
+}
+
+}  // namespace
+
+hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K,
+                           uint32_t* packed, float* row_abs, float* alpha, hipStream_t stream) {
+    compress_kernel<<<(rows + kWaves - 1) / kWaves, kWaves * 64, 0, stream>>>(fine, base, rows, K,
+                                                                              packed, row_abs);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || alpha == nullptr) return e;
+    mean_kernel<<<1, kMeanThreads, 0, stream>>>(row_abs, rows, (double)rows * (double)K, alpha);
+    return hipGetLastError();
+}
+
+}  // namespace bitdelta

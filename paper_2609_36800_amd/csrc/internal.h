@@ -19,6 +19,11 @@ hipError_t launch_pack(const void* signs, int dtype, int64_t elems, uint32_t* pa
 hipError_t launch_unpack(const uint32_t* packed, int64_t elems, void* signs, int dtype,
                          hipStream_t stream);
 
+// Binary delta of a fine-tuned weight: packed signs of W_fine - W_base, the
+// per-row sums of |delta| and (when alpha is not null) their mean.
+hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K,
+                           uint32_t* packed, float* row_abs, float* alpha, hipStream_t stream);
+
 // Single-tenant decode matmul for at most 16 rows (signs and x staged via LDS).
 hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,

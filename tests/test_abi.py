@@ -132,6 +132,28 @@ def test_pack_unpack_errors(lib):
     assert lib.bitdelta_unpack(A, 4, 0, B, bd.F32, None) == 0
 
 
+def test_compress_errors(lib):
+    F, Bs, Pk, R, Al = A, B, C, D, E
+    cp = lib.bitdelta_compress
+    assert cp(F, Bs, 4, 48, Pk, R, Al, None) == -2        # K % 32
+    assert cp(F, Bs, -1, 32, Pk, R, Al, None) == -2
+    assert cp(F, Bs, 4, -32, Pk, R, Al, None) == -2
+    assert cp(None, Bs, 4, 32, Pk, R, Al, None) == -1
+    assert cp(F, None, 4, 32, Pk, R, Al, None) == -1
+    assert cp(F, Bs, 4, 32, None, R, Al, None) == -1
+    assert cp(F, Bs, 4, 32, Pk, None, Al, None) == -1      # row sums are required
+    assert cp(F + 8, Bs, 4, 32, Pk, R, Al, None) == -3
+    assert cp(F, Bs + 2, 4, 32, Pk, R, Al, None) == -3
+    assert cp(F, Bs, 4, 32, Pk + 2, R, Al, None) == -3
+    assert cp(F, Bs, 4, 32, Pk, R + 1, Al, None) == -3
+    assert cp(F, Bs, 4, 32, Pk, R, Al + 2, None) == -3
+    assert cp(F, Bs, 4, 32, F + 64, R, Al, None) == -7     # packed inside w_fine
+    assert cp(F, Bs, 4, 32, Pk, Pk, Al, None) == -7        # row sums over packed
+    assert cp(F, Bs, 4, 32, Pk, R, R, None) == -7          # alpha over row sums
+    assert cp(F, Bs, 0, 32, Pk, R, Al, None) == 0
+    assert cp(F, Bs, 4, 0, Pk, R, Al, None) == 0
+
+
 def test_path_selection(lib):
     assert bd.matmul_path(1, 4096, 4096, 1, False) == bd.PATH_SKINNY
     assert bd.matmul_path(64, 4096, 4096, 1, False) == bd.PATH_SKINNY
