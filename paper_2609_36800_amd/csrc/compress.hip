@@ -16,12 +16,14 @@
 // (two 8-bit significands then span more than fp32's 24 bits).
 //
 // compress_kernel streams both weights once (HBM-bound: 4 bytes read per
-// element, 1/8 written): one wave per row, lane l taking 8 consecutive elements
-// of each 512-element chunk, so its 8 sign bits are byte l of the chunk's
-// packed words and a wave's byte stores cover 64 contiguous bytes.  Four
-// chunks are loaded before any is used.  The per-lane sums are added in a
-// fixed butterfly, so the result does not depend on scheduling.
-// mean_kernel (one workgroup) then reduces the per-row sums in a fixed order.
+// element, 1/8 written).  One 4-wave workgroup per row; wave w takes the
+// 512-element chunks w, w+4, ..., lane l the 8 consecutive elements 8l..8l+7
+// of a chunk, so its 8 sign bits are byte l of the chunk's packed words and a
+// wave's byte stores cover 64 contiguous bytes.  Up to four chunks per wave are
+// loaded before any is used.  Per-lane sums are added in a fixed butterfly and
+// the four wave sums in wave order, so the result does not depend on
+// scheduling.  mean_kernel (one workgroup) then reduces the per-row sums in a
+// fixed order.
 #include "device.h"
 #include "internal.h"
 
@@ -36,29 +38,29 @@ __device__ __forceinline__ float lo_f32(uint32_t v) { return __builtin_bit_cast(
 __device__ __forceinline__ float hi_f32(uint32_t v) { return __builtin_bit_cast(float, v & 0xFFFF0000u); }
 
 __global__ __launch_bounds__(kWaves * 64) void compress_kernel(
-    const uint16_t* __restrict__ fine, const uint16_t* __restrict__ base, int rows, int K,
+    const uint16_t* __restrict__ fine, const uint16_t* __restrict__ base, int K,
     uint32_t* __restrict__ packed, float* __restrict__ row_abs) {
-    const int lane = threadIdx.x & 63;
-    const int row = blockIdx.x * kWaves + (threadIdx.x >> 6);
-    if (row >= rows) return;  // whole waves leave; there is no barrier
+    __shared__ float wave_sum[kWaves];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int row = blockIdx.x;
     const uint16_t* f = fine + (size_t)row * K;
     const uint16_t* b = base + (size_t)row * K;
     uint8_t* out = reinterpret_cast<uint8_t*>(packed + (size_t)row * (K / 32));
 
     float acc = 0.f;
-    for (int k0 = 0; k0 < K; k0 += kChunk * kUnroll) {
+    for (int k0 = kChunk * wv; k0 < K; k0 += kChunk * kWaves * kUnroll) {
         u32x4 fv[kUnroll], bv[kUnroll];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int k = k0 + kChunk * u + 8 * lane;
+            const int k = k0 + kChunk * kWaves * u + 8 * lane;
             if (k < K) {
-                fv[u] = load16(f + k);
-                bv[u] = load16(b + k);
+                fv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(f + k));
+                bv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(b + k));
             }
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-            const int k = k0 + kChunk * u + 8 * lane;
+            const int k = k0 + kChunk * kWaves * u + 8 * lane;
             if (k >= K) continue;
             uint32_t byte = 0;
 #pragma unroll
@@ -75,32 +77,51 @@ __global__ __launch_bounds__(kWaves * 64) void compress_kernel(
     }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) acc += __shfl_xor(acc, d);
-    if (lane == 0) row_abs[row] = acc;
+    if (lane == 0) wave_sum[wv] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float s = wave_sum[0];
+#pragma unroll
+        for (int w = 1; w < kWaves; ++w) s += wave_sum[w];
+        row_abs[row] = s;
+    }
 }
 
-constexpr int kMeanThreads = 256;
+constexpr int kMeanThreads = 1024;
+constexpr int kMeanUnroll = 8;
 
 __global__ __launch_bounds__(kMeanThreads) void mean_kernel(const float* __restrict__ row_abs,
                                                             int rows, double count,
                                                             float* __restrict__ alpha) {
-    __shared__ double part[kMeanThreads];
+    __shared__ double wave_part[kMeanThreads / 64];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     double s = 0.0;
-    for (int i = threadIdx.x; i < rows; i += kMeanThreads) s += (double)row_abs[i];
-    part[threadIdx.x] = s;
-    __syncthreads();
-    for (int d = kMeanThreads / 2; d > 0; d >>= 1) {
-        if ((int)threadIdx.x < d) part[threadIdx.x] += part[threadIdx.x + d];
-        __syncthreads();
+    for (int i0 = 0; i0 < rows; i0 += kMeanThreads * kMeanUnroll) {
+        float v[kMeanUnroll];
+#pragma unroll
+        for (int u = 0; u < kMeanUnroll; ++u) {
+            const int i = i0 + kMeanThreads * u + (int)threadIdx.x;
+            v[u] = i < rows ? row_abs[i] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < kMeanUnroll; ++u) s += (double)v[u];
     }
-    if (threadIdx.x == 0) alpha[0] = (float)(part[0] / count);
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) s += __shfl_xor(s, d);
+    if (lane == 0) wave_part[wv] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = wave_part[0];
+        for (int w = 1; w < kMeanThreads / 64; ++w) t += wave_part[w];
+        alpha[0] = (float)(t / count);
+    }
 }
 
 }  // namespace
 
 hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K,
                            uint32_t* packed, float* row_abs, float* alpha, hipStream_t stream) {
-    compress_kernel<<<(rows + kWaves - 1) / kWaves, kWaves * 64, 0, stream>>>(fine, base, rows, K,
-                                                                              packed, row_abs);
+    compress_kernel<<<rows, kWaves * 64, 0, stream>>>(fine, base, K, packed, row_abs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || alpha == nullptr) return e;
     mean_kernel<<<1, kMeanThreads, 0, stream>>>(row_abs, rows, (double)rows * (double)K, alpha);

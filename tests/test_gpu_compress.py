@@ -20,9 +20,11 @@ def run(fine, base, with_alpha=True):
 
 
 def sum_bound(K):
-    # fp32 sums of nonnegative terms: K/64 sequential additions per lane, six
-    # butterfly levels, and at most one rounding of each |delta|
-    return (K / 64 + 8) * 2.0 ** -24
+    # fp32 sums of nonnegative terms: a lane adds 8 elements of every fourth
+    # 512-element chunk in sequence, then six butterfly levels and three
+    # additions of the wave sums; each |delta| is rounded at most once
+    per_lane = 8 * -(-K // 2048)
+    return (per_lane + 6 + 3 + 1) * 2.0 ** -24
 
 
 @pytest.mark.parametrize("rows,K", [(1, 32), (3, 96), (17, 2080), (64, 4096), (130, 11008),
