@@ -50,7 +50,8 @@ typedef enum {
 typedef enum {
     BITDELTA_F32 = 0,   /* IEEE binary32                  */
     BITDELTA_BF16 = 1,  /* bfloat16 bit patterns          */
-    BITDELTA_I8 = 2     /* signed 8-bit integers          */
+    BITDELTA_I8 = 2,    /* signed 8-bit integers          */
+    BITDELTA_F16 = 3    /* IEEE binary16 bit patterns     */
 } bitdelta_dtype;
 
 /* Kernel paths of bitdelta_matmul (see bitdelta_matmul_path). */
@@ -63,7 +64,7 @@ typedef enum {
 /*
  * Pack signs into bits (the storage format of the binary delta, Appendix A.2).
  *
- *   signs     [rows][K] of in_dtype (F32, BF16 or I8); alignment 4 * element size
+ *   signs     [rows][K] of in_dtype (F32, BF16, F16 or I8); alignment 4 * element size
  *   packed    [rows][K/32] uint32, 4-byte aligned
  *
  * Bit = 1 exactly when the element's sign bit is clear: +1 -> 1, -1 -> 0, and
@@ -78,7 +79,7 @@ int bitdelta_pack(const void* signs, int in_dtype, int64_t rows, int64_t K,
  * Decode packed bits into +1 / -1 (s = 2b - 1, Appendix A.2).
  *
  *   packed    [rows][K/32] uint32, 4-byte aligned
- *   signs     [rows][K] of out_dtype (F32, BF16 or I8); alignment 4 * element size
+ *   signs     [rows][K] of out_dtype (F32, BF16, F16 or I8); alignment 4 * element size
  *
  * Errors: NULL, SHAPE, ALIGN, DTYPE, HIP.
  */
@@ -99,18 +100,18 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K,
  * alpha is the least-squares scale for these signs: it minimises
  * ||delta - a * s||_F over a (the derivative vanishes at a = mean |delta|).
  *
- *   w_fine, w_base  [rows][K] bf16, 16-byte aligned
+ *   w_fine, w_base  [rows][K] of in_dtype (BF16 or F16), 16-byte aligned
  *   packed          [rows][K/32] uint32 output, 4-byte aligned
  *   row_abs_sum     [rows] fp32 output, 4-byte aligned (also holds the
  *                   partial sums of the alpha reduction)
  *   alpha           [1] fp32 output, or NULL to skip the mean
  *
- * Inputs are expected finite and free of bf16 subnormals.  rows == 0 or
- * K == 0 is a no-op.  Outputs must not overlap inputs or each other.
- * Errors: NULL, SHAPE (rows < 0, K < 0, K % 32), ALIGN, ALIAS, HIP.
+ * Inputs are expected finite and free of subnormals.  rows == 0 or K == 0
+ * is a no-op.  Outputs must not overlap inputs or each other.
+ * Errors: NULL, SHAPE (rows < 0, K < 0, K % 32), ALIGN, DTYPE, ALIAS, HIP.
  */
 int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base,
-                      int64_t rows, int64_t K, uint32_t* packed,
+                      int64_t rows, int64_t K, int in_dtype, uint32_t* packed,
                       float* row_abs_sum, float* alpha, hipStream_t stream);
 
 /*
@@ -157,6 +158,20 @@ int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K,
                               const uint32_t* packed_s, const float* alpha,
                               const int32_t* tenant_ids, int32_t T,
                               void* y, int y_dtype, int path, hipStream_t stream);
+
+/*
+ * The matmul with x and w_base of 16-bit type in_dtype: BITDELTA_BF16 (as
+ * bitdelta_matmul_with_path) or BITDELTA_F16, the paper's own precision for
+ * BitDelta (Appendix A.2).  y_dtype is F32 or in_dtype.  Everything else is
+ * as in bitdelta_matmul_with_path; for F16 the fused path's effective weight
+ * is fp16_rne(W_base + fp16_rne(+-alpha_t)), formed with packed fp16 adds.
+ * Errors: as bitdelta_matmul, DTYPE for any other in_dtype / y_dtype pair.
+ */
+int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K,
+                          const uint16_t* w_base, int64_t N,
+                          const uint32_t* packed_s, const float* alpha,
+                          const int32_t* tenant_ids, int32_t T, int in_dtype,
+                          void* y, int y_dtype, int path, hipStream_t stream);
 
 /* The path bitdelta_matmul picks for these sizes (no side effects). */
 int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids);

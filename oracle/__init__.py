@@ -65,10 +65,10 @@ def _load():
         f.restype = ctypes.c_int
     lib.oracle_unpack_f64.argtypes = [P, I64, I64, P]
     lib.oracle_unpack_f64.restype = ctypes.c_int
-    lib.oracle_compress.argtypes = [P, P, I64, I64, P, P, P]
+    lib.oracle_compress.argtypes = [P, P, I64, I64, ctypes.c_int, P, P, P]
     lib.oracle_compress.restype = ctypes.c_int
     lib.oracle_matmul_parts.argtypes = [P, I64, I64, P, I64, P, P, P, ctypes.c_int32,
-                                        P, I64, P, P, P]
+                                        P, I64, ctypes.c_int, P, P, P]
     lib.oracle_matmul_parts.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -120,10 +120,13 @@ def unpack(packed: np.ndarray, K: int) -> np.ndarray:
     return out
 
 
-def compress(fine_bits, base_bits):
+_DT = {"bf16": 1, "f16": 3}
+
+
+def compress(fine_bits, base_bits, dtype: str = "bf16"):
     """Binary delta of a fine-tuned weight against its base, in fp64.
 
-    fine_bits, base_bits  uint16 [rows, K] (bf16 bit patterns)
+    fine_bits, base_bits  uint16 [rows, K] (bf16 or fp16 bit patterns, per dtype)
     Returns (packed uint32 [rows, K/32], row_abs float64 [rows], alpha float):
     the packed signs of delta = fine - base (bit set when delta's sign bit is
     clear), sum_k |delta| per row, and alpha = mean |delta|, the scale that
@@ -140,18 +143,18 @@ def compress(fine_bits, base_bits):
     packed = np.zeros((rows, K // 32), dtype=np.uint32)
     row_abs = np.zeros(rows, dtype=np.float64)
     alpha = np.zeros(1, dtype=np.float64)
-    rc = lib.oracle_compress(_ptr(fine_bits), _ptr(base_bits), rows, K, _ptr(packed),
+    rc = lib.oracle_compress(_ptr(fine_bits), _ptr(base_bits), rows, K, _DT[dtype], _ptr(packed),
                              _ptr(row_abs), _ptr(alpha))
     if rc != 0:
         raise RuntimeError(f"oracle compress failed ({rc})")
     return packed, row_abs, float(alpha[0])
 
 
-def matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None):
+def matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None, dtype="bf16"):
     """fp64 evaluation of the binary-delta matmul.
 
-    x_bits  uint16 [M, K] (bf16 bit patterns)
-    w_bits  uint16 [N, K] (bf16 bit patterns)
+    x_bits  uint16 [M, K] (bf16 or fp16 bit patterns, per dtype)
+    w_bits  uint16 [N, K] (same type)
     packed  uint32 [T, N, K/32] (or [N, K/32] for one tenant)
     alpha   float32 [T]
     tenant_ids  int32 [M] or None (all rows use tenant 0)
@@ -189,13 +192,13 @@ def matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None):
     delta = np.empty((M, cnt), dtype=np.float64)
     y = np.empty((M, cnt), dtype=np.float64)
     rc = lib.oracle_matmul_parts(_ptr(x_bits), M, K, _ptr(w_bits), N, _ptr(packed),
-                                 _ptr(alpha), _ptr(tid), T, _ptr(idx), cnt,
+                                 _ptr(alpha), _ptr(tid), T, _ptr(idx), cnt, _DT[dtype],
                                  _ptr(base), _ptr(delta), _ptr(y))
     if rc != 0:
         raise RuntimeError(f"oracle matmul failed ({rc})")
     return base, delta, y
 
 
-def matmul(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None):
+def matmul(x_bits, w_bits, packed, alpha, tenant_ids=None, n_idx=None, dtype="bf16"):
     """y = x W^T + alpha_t x S_t^T in fp64 (see ``matmul_parts``)."""
-    return matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids, n_idx)[2]
+    return matmul_parts(x_bits, w_bits, packed, alpha, tenant_ids, n_idx, dtype)[2]

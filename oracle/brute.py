@@ -30,6 +30,21 @@ def bf16_bits_to_fraction(h: int) -> Fraction:
     return sign * val
 
 
+def f16_bits_to_fraction(h: int) -> Fraction:
+    """Exact value of an IEEE binary16 bit pattern (finite values only)."""
+    h &= 0xFFFF
+    sign = -1 if (h >> 15) & 1 else 1
+    exp = (h >> 10) & 0x1F
+    man = h & 0x3FF
+    if exp == 0x1F:
+        raise ValueError("non-finite fp16")
+    if exp == 0:
+        val = Fraction(man, 1 << 10) * Fraction(1, 1 << 14)
+    else:
+        val = (1 + Fraction(man, 1 << 10)) * (Fraction(2) ** (exp - 15))
+    return sign * val
+
+
 def f32_to_fraction(v: float) -> Fraction:
     """Exact value of a float32 (the float is first rounded to fp32)."""
     (bits,) = struct.unpack("<I", struct.pack("<f", v))
@@ -41,12 +56,14 @@ def sign_from_words(words, k: int) -> int:
     return 1 if (int(words[k // 32]) >> (k % 32)) & 1 else -1
 
 
-def matmul_exact(x_bits, w_bits, packed, alpha, tenant_ids=None):
+def matmul_exact(x_bits, w_bits, packed, alpha, tenant_ids=None, dtype="bf16"):
     """Exact y as a nested list of Fractions (None for out-of-range tenants).
 
-    x_bits [M][K] and w_bits [N][K] are bf16 bit patterns, packed is
-    [T][N][K/32] of uint32 words, alpha a length-T sequence of fp32 values.
+    x_bits [M][K] and w_bits [N][K] are bf16 (or, with dtype="f16", IEEE
+    binary16) bit patterns, packed is [T][N][K/32] of uint32 words, alpha a
+    length-T sequence of fp32 values.
     """
+    dec = f16_bits_to_fraction if dtype == "f16" else bf16_bits_to_fraction
     M = len(x_bits)
     K = len(x_bits[0]) if M else 0
     N = len(w_bits)
@@ -62,8 +79,8 @@ def matmul_exact(x_bits, w_bits, packed, alpha, tenant_ids=None):
             a = f32_to_fraction(float(alpha[t]))
             acc = Fraction(0)
             for k in range(K):
-                xv = bf16_bits_to_fraction(int(x_bits[m][k]))
-                wv = bf16_bits_to_fraction(int(w_bits[n][k]))
+                xv = dec(int(x_bits[m][k]))
+                wv = dec(int(w_bits[n][k]))
                 s = sign_from_words(packed[t][n], k)
                 acc += xv * wv + a * xv * s
             row.append(acc)

@@ -14,6 +14,8 @@
  *                 axis and bit order are this library's stated format.
  *   pack          bit = 1 exactly when the input's IEEE / two's-complement
  *                 sign bit is clear (so +1 -> 1, -1 -> 0).
+ *   inputs        x and W are bf16 or IEEE fp16 bit patterns, both decoded
+ *                 exactly to double.
  *   compress      delta = W_fine - W_base; packed = pack(delta); the scale is
  *                 the mean of |delta| (the least-squares scale for the signs).
  *   matmul        y[m][n] = sum_k x[m][k] W[n][k]
@@ -43,6 +45,24 @@ static double bf16_to_double(uint16_t h) {
     float f;
     memcpy(&f, &u, sizeof f);
     return (double)f;
+}
+
+/* IEEE binary16 bit pattern -> double (exact): sign, 5-bit exponent with
+ * bias 15, 10-bit fraction; exponent 0 holds the subnormals f * 2^-24. */
+static double f16_to_double(uint16_t h) {
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1F;
+    int f = h & 0x3FF;
+    double v;
+    if (e == 0) v = ldexp((double)f, -24);
+    else if (e == 31) v = f ? NAN : INFINITY;
+    else v = ldexp((double)(1024 + f), e - 25);
+    return sign ? -v : v;
+}
+
+/* 16-bit element -> double for element type code dt (1 = bf16, 3 = fp16). */
+static double elem_to_double(uint16_t h, int dt) {
+    return dt == 3 ? f16_to_double(h) : bf16_to_double(h);
 }
 
 /* Sign of weight (n, k) from the packed rows: +1 when the bit is set, else -1. */
@@ -140,8 +160,9 @@ int oracle_unpack_f64(const uint32_t* packed, int64_t rows, int64_t K, double* o
  * The binary delta the paper's kernel decodes (Appendix A.2) is this pair.
  */
 int oracle_compress(const uint16_t* fine, const uint16_t* base, int64_t rows, int64_t K,
-                    uint32_t* packed, double* row_abs, double* alpha) {
+                    int dt, uint32_t* packed, double* row_abs, double* alpha) {
     if (K % 32 != 0 || rows < 0 || K < 0) return -2;
+    if (dt != 1 && dt != 3) return -4;
     int64_t n = rows * K;
     uint8_t* sb = (uint8_t*)malloc((size_t)(n > 0 ? n : 1));
     if (!sb) return -7;
@@ -149,7 +170,7 @@ int oracle_compress(const uint16_t* fine, const uint16_t* base, int64_t rows, in
     for (int64_t r = 0; r < rows; ++r) {
         double acc = 0.0;
         for (int64_t k = 0; k < K; ++k) {
-            double d = bf16_to_double(fine[r * K + k]) - bf16_to_double(base[r * K + k]);
+            double d = elem_to_double(fine[r * K + k], dt) - elem_to_double(base[r * K + k], dt);
             sb[r * K + k] = (uint8_t)(signbit(d) ? 1 : 0);
             acc += fabs(d);
         }
@@ -168,7 +189,8 @@ int oracle_compress(const uint16_t* fine, const uint16_t* base, int64_t rows, in
  * Evaluates the output at rows m in [0, M) and at the n_count output features
  * listed in n_idx (all of [0, N) when n_idx == NULL, with n_count == N).
  *
- *   x         bf16 bits [M][K]           W     bf16 bits [N][K]
+ *   x         16-bit bits [M][K]         W     16-bit bits [N][K]
+ *   dt        element type of x and W: 1 = bf16, 3 = fp16 (IEEE binary16)
  *   packed    uint32 [T][N][K/32]        alpha fp32 [T]
  *   tenant    int32 [M] or NULL (every row uses tenant 0)
  *   base_out  optional fp64 [M][n_count]: sum_k x W
@@ -179,9 +201,10 @@ int oracle_matmul_parts(const uint16_t* x, int64_t M, int64_t K,
                         const uint16_t* W, int64_t N,
                         const uint32_t* packed, const float* alpha,
                         const int32_t* tenant, int32_t T,
-                        const int64_t* n_idx, int64_t n_count,
+                        const int64_t* n_idx, int64_t n_count, int dt,
                         double* base_out, double* delta_out, double* y_out) {
     if (K % 32 != 0 || M < 0 || N < 0 || K < 0 || T < 1 || n_count < 0) return -2;
+    if (dt != 1 && dt != 3) return -4;
     if (n_idx == NULL && n_count != N) return -2;
     int64_t words = K / 32;
     int64_t j;
@@ -200,8 +223,8 @@ int oracle_matmul_parts(const uint16_t* x, int64_t M, int64_t K,
             const uint32_t* srow = packed + ((int64_t)t * N + n) * words;
             double base = 0.0, delta = 0.0;
             for (int64_t k = 0; k < K; ++k) {
-                double xv = bf16_to_double(x[m * K + k]);
-                base += xv * bf16_to_double(W[n * K + k]);
+                double xv = elem_to_double(x[m * K + k], dt);
+                base += xv * elem_to_double(W[n * K + k], dt);
                 delta += xv * sign_at(srow, k);
             }
             if (base_out) base_out[o] = base;

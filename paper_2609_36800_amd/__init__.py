@@ -22,7 +22,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libbitdelta.so")
 
 OK = 0
-F32, BF16, I8 = 0, 1, 2
+F32, BF16, I8, F16 = 0, 1, 2, 3
 PATH_AUTO, PATH_SKINNY, PATH_PREFILL = 0, 1, 2
 
 EXPORTED = (
@@ -31,6 +31,7 @@ EXPORTED = (
     "bitdelta_compress",
     "bitdelta_matmul",
     "bitdelta_matmul_with_path",
+    "bitdelta_matmul_typed",
     "bitdelta_matmul_path",
     "bitdelta_status_string",
     "bitdelta_version",
@@ -60,12 +61,14 @@ def load_library(path: str = LIB_PATH):
     lib.bitdelta_pack.restype = I
     lib.bitdelta_unpack.argtypes = [P, I64, I64, P, I, P]
     lib.bitdelta_unpack.restype = I
-    lib.bitdelta_compress.argtypes = [P, P, I64, I64, P, P, P, P]
+    lib.bitdelta_compress.argtypes = [P, P, I64, I64, I, P, P, P, P]
     lib.bitdelta_compress.restype = I
     lib.bitdelta_matmul.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, P]
     lib.bitdelta_matmul.restype = I
     lib.bitdelta_matmul_with_path.argtypes = [P, I64, I64, P, I64, P, P, P, I32, P, I, I, P]
     lib.bitdelta_matmul_with_path.restype = I
+    lib.bitdelta_matmul_typed.argtypes = [P, I64, I64, P, I64, P, P, P, I32, I, P, I, I, P]
+    lib.bitdelta_matmul_typed.restype = I
     lib.bitdelta_matmul_path.argtypes = [I64, I64, I64, I32, I]
     lib.bitdelta_matmul_path.restype = I
     lib.bitdelta_status_string.argtypes = [I]
@@ -92,7 +95,7 @@ def _stream(t):
 
 def _dtype_code(dt):
     import torch
-    codes = {torch.float32: F32, torch.bfloat16: BF16, torch.int8: I8}
+    codes = {torch.float32: F32, torch.bfloat16: BF16, torch.int8: I8, torch.float16: F16}
     if dt not in codes:
         raise TypeError(f"unsupported dtype {dt}")
     return codes[dt]
@@ -108,9 +111,9 @@ def _dev(t, name, dtypes):
 
 
 def pack(signs, out=None):
-    """Pack signs [rows, K] (float32 / bfloat16 / int8) into int32 words [rows, K/32]."""
+    """Pack signs [rows, K] (float32 / bfloat16 / float16 / int8) into int32 words [rows, K/32]."""
     import torch
-    _dev(signs, "signs", (torch.float32, torch.bfloat16, torch.int8))
+    _dev(signs, "signs", (torch.float32, torch.bfloat16, torch.float16, torch.int8))
     rows, K = signs.shape
     if out is None:
         out = torch.empty((rows, K // 32), dtype=torch.int32, device=signs.device)
@@ -128,22 +131,22 @@ def unpack(packed, K: int, dtype=None, out=None):
     rows = packed.shape[0]
     if out is None:
         out = torch.empty((rows, K), dtype=dtype, device=packed.device)
-    _dev(out, "out", (torch.float32, torch.bfloat16, torch.int8))
+    _dev(out, "out", (torch.float32, torch.bfloat16, torch.float16, torch.int8))
     _check(load_library().bitdelta_unpack(packed.data_ptr(), rows, K, out.data_ptr(),
                                           _dtype_code(out.dtype), _stream(packed)))
     return out
 
 
 def compress(w_fine, w_base, with_alpha: bool = True):
-    """Binary delta of w_fine against w_base (both bf16 [rows, K]).
+    """Binary delta of w_fine against w_base (both bf16, or both float16, [rows, K]).
 
     Returns (packed int32 [rows, K/32], alpha fp32 [1] or None, row_abs_sum
     fp32 [rows]): the packed signs of w_fine - w_base, their least-squares
     scale mean|w_fine - w_base|, and the per-row sums of |w_fine - w_base|.
     """
     import torch
-    _dev(w_fine, "w_fine", (torch.bfloat16,))
-    _dev(w_base, "w_base", (torch.bfloat16,))
+    _dev(w_fine, "w_fine", (torch.bfloat16, torch.float16))
+    _dev(w_base, "w_base", (w_fine.dtype,))
     if w_fine.shape != w_base.shape or w_fine.dim() != 2:
         raise ValueError("w_fine and w_base must be [rows, K] of the same shape")
     rows, K = w_fine.shape
@@ -151,7 +154,8 @@ def compress(w_fine, w_base, with_alpha: bool = True):
     row_abs = torch.empty((rows,), dtype=torch.float32, device=w_fine.device)
     alpha = torch.empty((1,), dtype=torch.float32, device=w_fine.device) if with_alpha else None
     _check(load_library().bitdelta_compress(
-        w_fine.data_ptr(), w_base.data_ptr(), rows, K, packed.data_ptr(), row_abs.data_ptr(),
+        w_fine.data_ptr(), w_base.data_ptr(), rows, K, _dtype_code(w_fine.dtype), packed.data_ptr(),
+        row_abs.data_ptr(),
         None if alpha is None else alpha.data_ptr(), _stream(w_fine)))
     return packed, alpha, row_abs
 
@@ -160,13 +164,14 @@ def matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=None, out=None
            path: int = PATH_AUTO):
     """y = x W^T + alpha_t x S_t^T.
 
-    x [M, K] bf16, w_base [N, K] bf16, packed_s int32 [T, N, K/32] (or [N, K/32]),
-    alpha fp32 [T], tenant_ids int32 [M] or None, out_dtype float32 or bfloat16.
+    x [M, K] and w_base [N, K] both bfloat16 or both float16, packed_s int32
+    [T, N, K/32] (or [N, K/32]), alpha fp32 [T], tenant_ids int32 [M] or None,
+    out_dtype float32 or the input type (the default).
     """
     import torch
-    out_dtype = out_dtype or torch.bfloat16
-    _dev(x, "x", (torch.bfloat16,))
-    _dev(w_base, "w_base", (torch.bfloat16,))
+    _dev(x, "x", (torch.bfloat16, torch.float16))
+    _dev(w_base, "w_base", (x.dtype,))
+    out_dtype = out_dtype or x.dtype
     _dev(packed_s, "packed_s", (torch.int32,))
     _dev(alpha, "alpha", (torch.float32,))
     M, K = x.shape
@@ -185,10 +190,10 @@ def matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=None, out=None
         tptr = tenant_ids.data_ptr()
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=x.device)
-    _dev(out, "out", (torch.float32, torch.bfloat16))
-    _check(load_library().bitdelta_matmul_with_path(
+    _dev(out, "out", (torch.float32, x.dtype))
+    _check(load_library().bitdelta_matmul_typed(
         x.data_ptr(), M, K, w_base.data_ptr(), N, packed_s.data_ptr(), alpha.data_ptr(),
-        tptr, T, out.data_ptr(), _dtype_code(out.dtype), path, _stream(x)))
+        tptr, T, _dtype_code(x.dtype), out.data_ptr(), _dtype_code(out.dtype), path, _stream(x)))
     return out
 
 

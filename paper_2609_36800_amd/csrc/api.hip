@@ -21,6 +21,7 @@ int elem_size(int dtype) {
     switch (dtype) {
         case BITDELTA_F32: return 4;
         case BITDELTA_BF16: return 2;
+        case BITDELTA_F16: return 2;
         case BITDELTA_I8: return 1;
         default: return 0;
     }
@@ -39,11 +40,12 @@ constexpr int64_t kMaxDim = (int64_t)1 << 30;
 
 int check_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w, int64_t N,
                  const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
-                 int32_t T, void* y, int y_dtype) {
+                 int32_t T, int in_dtype, void* y, int y_dtype) {
     if (M < 0 || N < 0 || K < 0 || T < 1) return BITDELTA_ERR_SHAPE;
     if (K % 32 != 0) return BITDELTA_ERR_SHAPE;
     if (M > kMaxDim || N > kMaxDim || K > kMaxDim) return BITDELTA_ERR_SHAPE;
-    if (y_dtype != BITDELTA_F32 && y_dtype != BITDELTA_BF16) return BITDELTA_ERR_DTYPE;
+    if (in_dtype != BITDELTA_BF16 && in_dtype != BITDELTA_F16) return BITDELTA_ERR_DTYPE;
+    if (y_dtype != BITDELTA_F32 && y_dtype != in_dtype) return BITDELTA_ERR_DTYPE;
     if (M == 0 || N == 0) return BITDELTA_OK;
     if (y == nullptr || alpha == nullptr) return BITDELTA_ERR_NULL;
     if (K > 0 && (x == nullptr || w == nullptr || packed == nullptr)) return BITDELTA_ERR_NULL;
@@ -97,6 +99,8 @@ int bitdelta_pack(const void* signs, int in_dtype, int64_t rows, int64_t K, uint
     if (!aligned(signs, 4 * es) || !aligned(packed, 4)) return BITDELTA_ERR_ALIGN;
     if (overlaps(packed, (size_t)rows * (K / 32) * 4, signs, (size_t)rows * K * es))
         return BITDELTA_ERR_ALIAS;
+    // the sign bit of both 16-bit formats is bit 15: one kernel serves both
+    if (in_dtype == BITDELTA_F16) in_dtype = BITDELTA_BF16;
     return hip_status(bitdelta::launch_pack(signs, in_dtype, rows * K, packed, stream));
 }
 
@@ -114,7 +118,9 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K, void* signs
 }
 
 int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base, int64_t rows, int64_t K,
-                      uint32_t* packed, float* row_abs_sum, float* alpha, hipStream_t stream) {
+                      int in_dtype, uint32_t* packed, float* row_abs_sum, float* alpha,
+                      hipStream_t stream) {
+    if (in_dtype != BITDELTA_BF16 && in_dtype != BITDELTA_F16) return BITDELTA_ERR_DTYPE;
     if (rows < 0 || K < 0 || K % 32 != 0 || rows > kMaxDim || K > kMaxDim) return BITDELTA_ERR_SHAPE;
     if (rows == 0 || K == 0) return BITDELTA_OK;
     if (w_fine == nullptr || w_base == nullptr || packed == nullptr || row_abs_sum == nullptr)
@@ -130,7 +136,7 @@ int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base, int64_t ro
         overlaps(alpha, abytes, w_base, wbytes) || overlaps(alpha, abytes, packed, pbytes) ||
         overlaps(alpha, abytes, row_abs_sum, rbytes))
         return BITDELTA_ERR_ALIAS;
-    return hip_status(bitdelta::launch_compress(w_fine, w_base, (int)rows, (int)K, packed,
+    return hip_status(bitdelta::launch_compress(w_fine, w_base, (int)rows, (int)K, in_dtype, packed,
                                                 row_abs_sum, alpha, stream));
 }
 
@@ -138,11 +144,11 @@ int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_ten
     return choose_path(M, N, K, T, has_tenant_ids);
 }
 
-int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
-                              int64_t N, const uint32_t* packed_s, const float* alpha,
-                              const int32_t* tenant_ids, int32_t T, void* y, int y_dtype,
-                              int path, hipStream_t stream) {
-    int rc = check_matmul(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, y, y_dtype);
+int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
+                          int64_t N, const uint32_t* packed_s, const float* alpha,
+                          const int32_t* tenant_ids, int32_t T, int in_dtype, void* y,
+                          int y_dtype, int path, hipStream_t stream) {
+    int rc = check_matmul(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, in_dtype, y, y_dtype);
     if (rc != BITDELTA_OK) return rc;
     if (path == BITDELTA_PATH_AUTO) path = choose_path(M, N, K, T, tenant_ids != nullptr);
     if (path != BITDELTA_PATH_SKINNY && path != BITDELTA_PATH_PREFILL) return BITDELTA_ERR_UNSUPPORTED;
@@ -150,14 +156,15 @@ int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uin
         !bitdelta::prefill_grouped_supported((int)M, (int)N, (int)K, T))
         return BITDELTA_ERR_UNSUPPORTED;
     if (M == 0 || N == 0) return BITDELTA_OK;
+    const int et = in_dtype;
 
     if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr)
         return hip_status(bitdelta::launch_prefill_grouped(x, (int)M, (int)K, w_base, (int)N,
                                                            packed_s, alpha, tenant_ids, (int)T, y,
-                                                           y_dtype, stream));
+                                                           y_dtype, et, stream));
     if (path == BITDELTA_PATH_PREFILL)
         return hip_status(bitdelta::launch_prefill(x, (int)M, (int)K, w_base, (int)N, packed_s,
-                                                   alpha, y, y_dtype, stream));
+                                                   alpha, y, y_dtype, et, stream));
 
     // Skinny path: 64 rows per launch (each launch streams W once more).
     const int es = elem_size(y_dtype);
@@ -166,17 +173,25 @@ int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uin
         rc = hip_status(bitdelta::launch_skinny(
             x + r0 * K, rows, (int)K, w_base, (int)N, packed_s, alpha,
             tenant_ids ? tenant_ids + r0 : nullptr, (int)T,
-            static_cast<char*>(y) + r0 * N * es, y_dtype, stream));
+            static_cast<char*>(y) + r0 * N * es, y_dtype, et, stream));
         if (rc != BITDELTA_OK) return rc;
     }
     return BITDELTA_OK;
 }
 
+int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
+                              int64_t N, const uint32_t* packed_s, const float* alpha,
+                              const int32_t* tenant_ids, int32_t T, void* y, int y_dtype,
+                              int path, hipStream_t stream) {
+    return bitdelta_matmul_typed(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, BITDELTA_BF16,
+                                 y, y_dtype, path, stream);
+}
+
 int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base, int64_t N,
                     const uint32_t* packed_s, const float* alpha, const int32_t* tenant_ids,
                     int32_t T, void* y, int y_dtype, hipStream_t stream) {
-    return bitdelta_matmul_with_path(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, y,
-                                     y_dtype, BITDELTA_PATH_AUTO, stream);
+    return bitdelta_matmul_typed(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, BITDELTA_BF16,
+                                 y, y_dtype, BITDELTA_PATH_AUTO, stream);
 }
 
 }  // extern "C"

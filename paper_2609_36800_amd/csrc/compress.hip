@@ -10,10 +10,10 @@
 // minimises sum (delta - a s)^2 satisfies sum s (delta - a s) = 0, and
 // s * s = 1, s * delta = |delta| give a = mean |delta|.
 //
-// The difference of two bf16 values has the exact sign in fp32 (a nonzero
-// difference is at least 2^-133 in magnitude, far above fp32's smallest
-// subnormal), and is exact itself unless the exponents differ by more than 15
-// (two 8-bit significands then span more than fp32's 24 bits).
+// The difference of two bf16 (or fp16) values has the exact sign in fp32 (a
+// nonzero difference is at least 2^-133 (2^-24) in magnitude, above fp32's
+// smallest subnormal), and is exact itself unless the exponents differ by more
+// than 15 (12 for fp16): the two significands then span more than 24 bits.
 //
 // compress_kernel streams both weights once (HBM-bound: 4 bytes read per
 // element, 1/8 written).  One 4-wave workgroup per row; wave w takes the
@@ -34,9 +34,19 @@ constexpr int kWaves = 4;
 constexpr int kChunk = 512;  // elements per wave-wide 16-byte load
 constexpr int kUnroll = 4;
 
-__device__ __forceinline__ float lo_f32(uint32_t v) { return __builtin_bit_cast(float, v << 16); }
-__device__ __forceinline__ float hi_f32(uint32_t v) { return __builtin_bit_cast(float, v & 0xFFFF0000u); }
+// The two 16-bit values of a dword as fp32 (exact).
+template <int ET>
+__device__ __forceinline__ float lo_f32(uint32_t v) {
+    if constexpr (ET == kF16) return (float)__builtin_bit_cast(f16x2, v)[0];
+    else return __builtin_bit_cast(float, v << 16);
+}
+template <int ET>
+__device__ __forceinline__ float hi_f32(uint32_t v) {
+    if constexpr (ET == kF16) return (float)__builtin_bit_cast(f16x2, v)[1];
+    else return __builtin_bit_cast(float, v & 0xFFFF0000u);
+}
 
+template <int ET>
 __global__ __launch_bounds__(kWaves * 64) void compress_kernel(
     const uint16_t* __restrict__ fine, const uint16_t* __restrict__ base, int K,
     uint32_t* __restrict__ packed, float* __restrict__ row_abs) {
@@ -65,8 +75,8 @@ __global__ __launch_bounds__(kWaves * 64) void compress_kernel(
             uint32_t byte = 0;
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                const float dl = lo_f32(fv[u][p]) - lo_f32(bv[u][p]);
-                const float dh = hi_f32(fv[u][p]) - hi_f32(bv[u][p]);
+                const float dl = lo_f32<ET>(fv[u][p]) - lo_f32<ET>(bv[u][p]);
+                const float dh = hi_f32<ET>(fv[u][p]) - hi_f32<ET>(bv[u][p]);
                 byte |= ((~__builtin_bit_cast(uint32_t, dl)) >> 31) << (2 * p);
                 byte |= ((~__builtin_bit_cast(uint32_t, dh)) >> 31) << (2 * p + 1);
                 acc += __builtin_fabsf(dl);
@@ -119,9 +129,12 @@ __global__ __launch_bounds__(kMeanThreads) void mean_kernel(const float* __restr
 
 }  // namespace
 
-hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K,
+hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K, int et,
                            uint32_t* packed, float* row_abs, float* alpha, hipStream_t stream) {
-    compress_kernel<<<rows, kWaves * 64, 0, stream>>>(fine, base, K, packed, row_abs);
+    if (et == kF16)
+        compress_kernel<kF16><<<rows, kWaves * 64, 0, stream>>>(fine, base, K, packed, row_abs);
+    else
+        compress_kernel<kBF16><<<rows, kWaves * 64, 0, stream>>>(fine, base, K, packed, row_abs);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || alpha == nullptr) return e;
     mean_kernel<<<1, kMeanThreads, 0, stream>>>(row_abs, rows, (double)rows * (double)K, alpha);

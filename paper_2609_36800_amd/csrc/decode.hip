@@ -48,7 +48,7 @@ __device__ __forceinline__ u32x4 lds_read16(const char* p) {
     return *reinterpret_cast<const u32x4*>(p);
 }
 
-template <int XR>
+template <int ET, int XR>
 __global__ __launch_bounds__(kWaves * 64) void decode_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -117,8 +117,8 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(
         auto consume = [&](int j) {
             const u32x4 xa = lds_read16(xs + xrow_lds * L::kXStride + j * 64 + 16 * g);
             const uint32_t sb = *reinterpret_cast<const uint8_t*>(ss + nl * kSignStride + 4 * j + g);
-            accb = mfma16(xa, wf[j], accb);
-            accs = mfma16(xa, decode_signs8(sb), accs);
+            accb = mfma16<ET>(xa, wf[j], accb);
+            accs = mfma16<ET>(xa, decode_signs8<ET>(sb), accs);
         };
         if (c == kRound) {
 #pragma unroll
@@ -151,10 +151,7 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(
                 s += red_s[(v * 16 + m) * kFeat + f];
             }
             const float out = __builtin_fmaf(alpha[0], s, b);
-            if (y_dtype == kF32)
-                reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
-            else
-                reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+            store_y<ET>(y, (size_t)m * N + nn, out, y_dtype);
         }
     }
 }
@@ -189,7 +186,7 @@ struct StreamCfg {
 __device__ __forceinline__ int tswz(int row, int chunk) { return chunk ^ (row & 15); }
 
 // SB: bytes reserved for the staged signs (16 features x K/8 bytes).
-template <int XR, int SB, bool XUP>
+template <int ET, int XR, int SB, bool XUP>
 __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -277,8 +274,8 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
                                  : *reinterpret_cast<const u32x4*>(buf + xoff);
             const uint32_t sb = *reinterpret_cast<const uint8_t*>(
                 sg + (kb >> 2) * 256 + nl * 16 + 4 * (kb & 3) + g);
-            accb = mfma16(xa, bw, accb);
-            accs = mfma16(xa, decode_signs8(sb), accs);
+            accb = mfma16<ET>(xa, bw, accb);
+            accs = mfma16<ET>(xa, decode_signs8<ET>(sb), accs);
         }
     }
     wait_vm_lgkm0<0>();
@@ -304,29 +301,46 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
                 s += red_s[(v * 16 + m) * kFeat + f];
             }
             const float out = __builtin_fmaf(alpha[0], s, b);
-            if (y_dtype == kF32)
-                reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
-            else
-                reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+            store_y<ET>(y, (size_t)m * N + nn, out, y_dtype);
         }
     }
 }
 
-template <int XR>
+template <int ET, int XR>
 hipError_t launch_stream(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                          hipStream_t stream) {
     const int grid = (N + kFeat - 1) / kFeat;
     if constexpr (XR <= 4) {
         if (K <= 4096) {
-            stream_decode_kernel<XR, 8192, true><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+            stream_decode_kernel<ET, XR, 8192, true><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
             return hipGetLastError();
         }
     }
     if (K <= 4096)
-        stream_decode_kernel<XR, 8192, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+        stream_decode_kernel<ET, XR, 8192, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
     else
-        stream_decode_kernel<XR, 32768, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+        stream_decode_kernel<ET, XR, 32768, false><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    return hipGetLastError();
+}
+
+template <int ET>
+hipError_t launch_decode_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                            const uint32_t* packed, const float* alpha, void* y, int y_dtype,
+                            hipStream_t stream) {
+    if (K >= 128 && (K & 127) == 0 && K <= 16384) {
+        // signs of 16 features x K fit the staging area; rows of W split into whole chunks
+        if (M == 1) return launch_stream<ET, 1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+        if (M <= 4) return launch_stream<ET, 4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+        return launch_stream<ET, 16>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+    }
+    const int grid = (N + kFeat - 1) / kFeat;
+    if (M == 1)
+        decode_kernel<ET, 1><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    else if (M <= 4)
+        decode_kernel<ET, 4><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
+    else
+        decode_kernel<ET, 16><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
     return hipGetLastError();
 }
 
@@ -334,21 +348,9 @@ hipError_t launch_stream(const uint16_t* x, int M, int K, const uint16_t* w, int
 
 hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
-                         hipStream_t stream) {
-    if (K >= 128 && (K & 127) == 0 && K <= 16384) {
-        // signs of 16 features x K fit the staging area; rows of W split into whole chunks
-        if (M == 1) return launch_stream<1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-        if (M <= 4) return launch_stream<4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-        return launch_stream<16>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-    }
-    const int grid = (N + kFeat - 1) / kFeat;
-    if (M == 1)
-        decode_kernel<1><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
-    else if (M <= 4)
-        decode_kernel<4><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
-    else
-        decode_kernel<16><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype);
-    return hipGetLastError();
+                         int et, hipStream_t stream) {
+    if (et == kF16) return launch_decode_et<kF16>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+    return launch_decode_et<kBF16>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
 }
 
 }  // namespace bitdelta

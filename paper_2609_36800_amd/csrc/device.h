@@ -16,39 +16,56 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "internal.h"
+
 namespace bitdelta {
 
+// Kernels templated on ET (the 16-bit element type of x and W: kBF16 or
+// kF16) use the matching matrix instruction, +-1 constant and rounding.
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(_Float16)))) _Float16 f16x8;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
 
-// bf16 pair (-1, -1): 0xBF80 in each half.  Clearing a half's sign bit (bit 15
-// or bit 31) turns that half into +1 (0x3F80).
-constexpr uint32_t kMinusOnePair = 0xBF80BF80u;
+// Pair (-1, -1) of the element type: 0xBF80 (bf16) or 0xBC00 (fp16) in each
+// half.  Clearing a half's sign bit (bit 15 or bit 31) turns it into +1.
+template <int ET>
+constexpr uint32_t kMinusOnePair = ET == kF16 ? 0xBC00BC00u : 0xBF80BF80u;
 constexpr uint32_t kSignBits = 0x80008000u;
 
+template <int ET>
 __device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    if constexpr (ET == kF16)
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+template <int ET>
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    if constexpr (ET == kF16)
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                      __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// Eight sign bits (bit i <-> slot i, bit 1 = +1) -> eight bf16 +1/-1 in slot order.
+// Eight sign bits (bit i <-> slot i, bit 1 = +1) -> eight +1/-1 in slot order.
 // The byte is first duplicated 15 bits higher, so one left shift brings bit 2j
 // to position 15 and bit 2j+1 to position 31 at once; one 3-input bit op then
 // flips the sign bits of the packed (-1, -1) constant: two values per two ops.
+template <int ET>
 __device__ __forceinline__ u32x4 decode_signs8(uint32_t byte) {
     const uint32_t s = byte | (byte << 15);
     u32x4 r;
-    r[0] = kMinusOnePair ^ ((s << 15) & kSignBits);
-    r[1] = kMinusOnePair ^ ((s << 13) & kSignBits);
-    r[2] = kMinusOnePair ^ ((s << 11) & kSignBits);
-    r[3] = kMinusOnePair ^ ((s << 9) & kSignBits);
+    r[0] = kMinusOnePair<ET> ^ ((s << 15) & kSignBits);
+    r[1] = kMinusOnePair<ET> ^ ((s << 13) & kSignBits);
+    r[2] = kMinusOnePair<ET> ^ ((s << 11) & kSignBits);
+    r[3] = kMinusOnePair<ET> ^ ((s << 9) & kSignBits);
     return r;
 }
 
@@ -71,9 +88,44 @@ __device__ __forceinline__ u32x4 fuse_weights8(u32x4 w, uint32_t byte, uint32_t 
     return r;
 }
 
+// fp16 flavour: the pair (-a, -a) holds fp16(-alpha) twice; a set bit flips a
+// half's sign to +a, and one packed fp16 add (nearest even) gives
+// fp16(w + (bit ? a : -a)) for two weights at once.
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, a) + __builtin_bit_cast(f16x2, b));
+}
+
+__device__ __forceinline__ u32x4 fuse_weights8_f16(u32x4 w, uint32_t byte, uint32_t neg_alpha_pair) {
+    const uint32_t s = byte | (byte << 15);
+    u32x4 r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = add_f16x2(w[j], neg_alpha_pair ^ ((s << (15 - 2 * j)) & kSignBits));
+    return r;
+}
+
 // fp32 -> bf16 round-to-nearest-even (quiet NaN stays NaN).
 __device__ __forceinline__ uint16_t to_bf16(float f) {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// fp32 -> fp16 round-to-nearest-even (overflow to inf, NaN stays NaN).
+__device__ __forceinline__ uint16_t to_f16(float f) {
+    return __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+}
+
+template <int ET>
+__device__ __forceinline__ uint16_t to_half(float f) {
+    if constexpr (ET == kF16) return to_f16(f);
+    else return to_bf16(f);
+}
+
+// Output element m*N+n of a y of dtype y_dtype (kF32, or the 16-bit ET).
+template <int ET>
+__device__ __forceinline__ void store_y(void* y, size_t i, float v, int y_dtype) {
+    if (y_dtype == kF32) reinterpret_cast<float*>(y)[i] = v;
+    else reinterpret_cast<uint16_t*>(y)[i] = to_half<ET>(v);
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {

@@ -7,10 +7,13 @@
 
 namespace bitdelta {
 
-// Element dtype codes (same values as the public bitdelta_dtype).
+// Element dtype codes (same values as the public bitdelta_dtype).  The matmul
+// launchers take `et`, the 16-bit type of x and W (kBF16 or kF16); a 16-bit
+// y has that same type.
 constexpr int kF32 = 0;
 constexpr int kBF16 = 1;
 constexpr int kI8 = 2;
+constexpr int kF16 = 3;
 
 // Pack / unpack over a flat run of `elems` elements (a multiple of 32): the
 // packed words of consecutive rows are contiguous, so rows need no special care.
@@ -21,32 +24,32 @@ hipError_t launch_unpack(const uint32_t* packed, int64_t elems, void* signs, int
 
 // Binary delta of a fine-tuned weight: packed signs of W_fine - W_base, the
 // per-row sums of |delta| and (when alpha is not null) their mean.
-hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K,
+hipError_t launch_compress(const uint16_t* fine, const uint16_t* base, int rows, int K, int et,
                            uint32_t* packed, float* row_abs, float* alpha, hipStream_t stream);
 
 // Single-tenant decode matmul for at most 16 rows (signs and x staged via LDS).
 hipError_t launch_decode(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha, void* y, int y_dtype,
-                         hipStream_t stream);
+                         int et, hipStream_t stream);
 
 // Batched (multi-tenant) matmul for at most 64 rows, operands staged in LDS by
 // global->LDS copies; needs K a positive multiple of 128 (multi_supported).
 bool multi_supported(int K);
 hipError_t launch_multi(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                         const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
-                        int T, void* y, int y_dtype, hipStream_t stream);
+                        int T, void* y, int y_dtype, int et, hipStream_t stream);
 
 // Decode-shaped matmul for at most 64 rows (any number of tenants).
 hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha,
-                         const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                         const int32_t* tenant_ids, int T, void* y, int y_dtype, int et,
                          hipStream_t stream);
 
 // Prefill-shaped single-tenant matmul: one bf16 GEMM over W + alpha*s.
 bool prefill_stream_supported(int M, int N, int K);
 hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                           const uint32_t* packed, const float* alpha, void* y, int y_dtype,
-                          hipStream_t stream);
+                          int et, hipStream_t stream);
 
 // Prefill-shaped batched matmul: one fused GEMM per tenant over its rows,
 // routed on the device; needs prefill_grouped_supported.
@@ -54,6 +57,6 @@ bool prefill_grouped_supported(int M, int N, int K, int T);
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,
                                   const int32_t* tenant_ids, int T, void* y, int y_dtype,
-                                  hipStream_t stream);
+                                  int et, hipStream_t stream);
 
 }  // namespace bitdelta

@@ -69,7 +69,7 @@ constexpr int pass_slots() { return MB <= 2 ? 16 : 8; }
 
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ (row & 15); }
 
-template <int MB>
+template <int ET, int MB>
 __global__ __launch_bounds__(kWaves * 64, 2) void multi_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kWaves * 64, 2) void multi_kernel(
                     if (first_pass) {
                         const u32x4 bw = *reinterpret_cast<const u32x4*>(buf + woff);
 #pragma unroll
-                        for (int mb = 0; mb < MB; ++mb) accb[mb] = mfma16(xa[mb], bw, accb[mb]);
+                        for (int mb = 0; mb < MB; ++mb) accb[mb] = mfma16<ET>(xa[mb], bw, accb[mb]);
                     }
                     // slots in chunks: the chunk's sign-byte reads first, then
                     // its decodes and MFMAs
@@ -234,9 +234,9 @@ __global__ __launch_bounds__(kWaves * 64, 2) void multi_kernel(
                             sb[i] = *reinterpret_cast<const uint8_t*>(sl + (s0 + i) * kSlotBytes + soff);
 #pragma unroll
                         for (int i = 0; i < CH; ++i) {
-                            const u32x4 bs = decode_signs8(sb[i]);
+                            const u32x4 bs = decode_signs8<ET>(sb[i]);
 #pragma unroll
-                            for (int mb = 0; mb < MB; ++mb) accs[s0 + i][mb] = mfma16(xa[mb], bs, accs[s0 + i][mb]);
+                            for (int mb = 0; mb < MB; ++mb) accs[s0 + i][mb] = mfma16<ET>(xa[mb], bs, accs[s0 + i][mb]);
                         }
                     }
                 }
@@ -303,21 +303,30 @@ __global__ __launch_bounds__(kWaves * 64, 2) void multi_kernel(
             for (int v = 0; v < kWaves; ++v) b += red[(v * kRowsMax + m) * kFeat + f];
             out = __builtin_fmaf(alpha[t], sign_sum[m][f], b);
         }
-        if (y_dtype == kF32)
-            reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
-        else
-            reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+        store_y<ET>(y, (size_t)m * N + nn, out, y_dtype);
     }
 }
 
-template <int MB>
+template <int ET, int MB>
 hipError_t launch_mb(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                      const uint32_t* packed, const float* alpha, const int32_t* tenant_ids, int T,
                      void* y, int y_dtype, hipStream_t stream) {
     const int grid = (N + kFeat - 1) / kFeat;
-    multi_kernel<MB><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, tenant_ids,
+    multi_kernel<ET, MB><<<grid, kWaves * 64, 0, stream>>>(x, M, K, w, N, packed, alpha, tenant_ids,
                                                        T, y, y_dtype);
     return hipGetLastError();
+}
+
+template <int ET>
+hipError_t launch_multi_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                           const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
+                           int T, void* y, int y_dtype, hipStream_t stream) {
+    switch ((M + 15) / 16) {
+        case 1: return launch_mb<ET, 1>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        case 2: return launch_mb<ET, 2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        case 3: return launch_mb<ET, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        default: return launch_mb<ET, 4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    }
 }
 
 }  // namespace
@@ -326,13 +335,10 @@ bool multi_supported(int K) { return K >= 128 && (K & 127) == 0; }
 
 hipError_t launch_multi(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                         const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
-                        int T, void* y, int y_dtype, hipStream_t stream) {
-    switch ((M + 15) / 16) {
-        case 1: return launch_mb<1>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        case 2: return launch_mb<2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        case 3: return launch_mb<3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        default: return launch_mb<4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-    }
+                        int T, void* y, int y_dtype, int et, hipStream_t stream) {
+    if (et == kF16)
+        return launch_multi_et<kF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    return launch_multi_et<kBF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
 }
 
 }  // namespace bitdelta

@@ -64,10 +64,12 @@ __global__ __launch_bounds__(kThreads) void unpack_kernel(const uint32_t* __rest
 #pragma unroll
             for (int i = 0; i < 4; ++i) v[i] = ((nib >> i) & 1u) ? 0x3F800000u : 0xBF800000u;
             reinterpret_cast<u32x4*>(dst)[q] = v;
-        } else if constexpr (DT == kBF16) {
+        } else if constexpr (DT == kBF16 || DT == kF16) {
+            constexpr uint32_t kPlus = DT == kF16 ? 0x3C00u : 0x3F80u;
+            constexpr uint32_t kMinus = kPlus | 0x8000u;
             uint2 v;
-            v.x = (((nib >> 0) & 1u) ? 0x3F80u : 0xBF80u) | ((((nib >> 1) & 1u) ? 0x3F80u : 0xBF80u) << 16);
-            v.y = (((nib >> 2) & 1u) ? 0x3F80u : 0xBF80u) | ((((nib >> 3) & 1u) ? 0x3F80u : 0xBF80u) << 16);
+            v.x = (((nib >> 0) & 1u) ? kPlus : kMinus) | ((((nib >> 1) & 1u) ? kPlus : kMinus) << 16);
+            v.y = (((nib >> 2) & 1u) ? kPlus : kMinus) | ((((nib >> 3) & 1u) ? kPlus : kMinus) << 16);
             reinterpret_cast<uint2*>(dst)[q] = v;
         } else {
             uint32_t v = 0;
@@ -107,6 +109,8 @@ hipError_t launch_unpack(const uint32_t* packed, int64_t elems, void* signs, int
         unpack_kernel<kF32><<<grid, kThreads, 0, stream>>>(packed, quads, signs);
     else if (dtype == kBF16)
         unpack_kernel<kBF16><<<grid, kThreads, 0, stream>>>(packed, quads, signs);
+    else if (dtype == kF16)
+        unpack_kernel<kF16><<<grid, kThreads, 0, stream>>>(packed, quads, signs);
     else
         unpack_kernel<kI8><<<grid, kThreads, 0, stream>>>(packed, quads, signs);
     return hipGetLastError();

@@ -64,6 +64,7 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
     return row * BK + ((chunk ^ (row & 7) ^ ((row >> 3) & 1)) << 3);
 }
 
+template <int ET>
 __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -86,7 +87,14 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
     const int wm = wv >> 1, wn = wv & 1;
     const int KW = K >> 5;
     const int KT = (K + BK - 1) / BK;
-    const uint32_t neg_alpha = __builtin_bit_cast(uint32_t, -alpha[0]);
+    // bf16: fp32 bits of -alpha; fp16: the pair (fp16(-alpha), fp16(-alpha))
+    uint32_t neg_alpha;
+    if constexpr (ET == kF16) {
+        const uint32_t h = to_f16(-alpha[0]);
+        neg_alpha = h | (h << 16);
+    } else {
+        neg_alpha = __builtin_bit_cast(uint32_t, -alpha[0]);
+    }
 
     // ---- global -> register staging assignment ----
     const int q = tid & 7, r0 = tid >> 3;
@@ -123,7 +131,10 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
             const int row = r0 + 32 * i;
             const int off = lds_off(row, q);
             *reinterpret_cast<u32x4*>(&lds.a[buf][off]) = ra[i];
-            const u32x4 fused = fuse_weights8(rb[i], (rs[i] >> (8 * (q & 3))) & 0xFFu, neg_alpha);
+            const uint32_t byte = (rs[i] >> (8 * (q & 3))) & 0xFFu;
+            u32x4 fused;
+            if constexpr (ET == kF16) fused = fuse_weights8_f16(rb[i], byte, neg_alpha);
+            else fused = fuse_weights8(rb[i], byte, neg_alpha);
             *reinterpret_cast<u32x4*>(&lds.b[buf][off]) = (vb[i] && kv) ? fused : zero;
         }
     };
@@ -154,7 +165,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
 #pragma unroll
             for (int i = 0; i < 4; ++i)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(af[i], bf[j], acc[i][j]);
+                for (int j = 0; j < 4; ++j) acc[i][j] = mfma32<ET>(af[i], bf[j], acc[i][j]);
         }
     };
 
@@ -180,12 +191,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_general_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int row = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (row < M && col < N) {
-                    if (y_dtype == kF32)
-                        reinterpret_cast<float*>(y)[(size_t)row * N + col] = acc[i][j][r];
-                    else
-                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
-                }
+                if (row < M && col < N) store_y<ET>(y, (size_t)row * N + col, acc[i][j][r], y_dtype);
             }
         }
 }
@@ -311,7 +317,7 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
 
 // Rows whose tenant id lies outside [0, T) are written as quiet NaN, columns
 // [n0, n0 + 256) (one workgroup per column tile).
-template <int YDT>
+template <int ET, int YDT>
 __device__ void write_invalid_rows(const int32_t* __restrict__ ids, int M, int T, int N, int n0,
                                    void* __restrict__ y) {
     const int lane = threadIdx.x & 63;
@@ -337,7 +343,7 @@ __device__ void write_invalid_rows(const int32_t* __restrict__ ids, int M, int T
                     if constexpr (YDT == kF32)
                         reinterpret_cast<float*>(y)[(size_t)r * N + col] = __builtin_nanf("");
                     else
-                        reinterpret_cast<uint16_t*>(y)[(size_t)r * N + col] = to_bf16(__builtin_nanf(""));
+                        reinterpret_cast<uint16_t*>(y)[(size_t)r * N + col] = to_half<ET>(__builtin_nanf(""));
                 }
             }
         }
@@ -393,12 +399,28 @@ __device__ __forceinline__ uint32_t fuse_pair(uint32_t w, uint32_t s, int p, flo
     return fuse_pair_b(fuse_pair_a(w, s, p), neg_alpha);
 }
 
-// YDT: output dtype; ALIGNED: output rows start on 16-byte boundaries (N a
-// multiple of 8 for bf16, of 4 for fp32), which allows 16-byte stores.
+// fp16 pair: fp16 has a packed add, so the whole pair is three operations: the
+// shift, one bit operation that moves the signs onto the (-a, -a) pair, and
+// v_pk_add_f16 (nearest even): fp16(w + fp16(+-alpha)).
+__device__ __forceinline__ uint32_t fuse_pair_f16(uint32_t w, uint32_t s, int p,
+                                                  uint32_t neg_alpha_pair) {
+    return add_f16x2(w, neg_alpha_pair ^ ((s << (15 - 2 * p)) & kSignBits));
+}
+
+// Two fp32 values -> one dword of two 16-bit outputs (nearest even).
+template <int ET>
+__device__ __forceinline__ uint32_t cvt_pair(f32x2v f) {
+    if constexpr (ET == kF16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2));
+    else return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2v));
+}
+
+// ET: 16-bit type of x and W; YDT: output dtype (kF32 or ET); ALIGNED: output
+// rows start on 16-byte boundaries (N a multiple of 8 for 16-bit outputs, of 4
+// for fp32), which allows 16-byte stores.
 // GROUPED: the batched form (tenant id per row, at most kMaxGroupedTenants
 // tenants); tiles_m is then the upper bound on the number of row tiles, and
 // tiles_n more workgroups past tiles_m * tiles_n write the rows of invalid ids.
-template <int YDT, bool ALIGNED, bool GROUPED>
+template <int ET, int YDT, bool ALIGNED, bool GROUPED>
 __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha_p,
@@ -414,7 +436,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     int tile_m = 0, tile_n, tenant = 0;
     if constexpr (GROUPED) {
         if ((int)blockIdx.x >= tiles_m * tiles_n) {
-            write_invalid_rows<YDT>(ids, M, T, N, ((int)blockIdx.x - tiles_m * tiles_n) * BN, y);
+            write_invalid_rows<ET, YDT>(ids, M, T, N, ((int)blockIdx.x - tiles_m * tiles_n) * BN, y);
             return;
         }
         if (!route_rows(ids, M, T, tiles_n, blockIdx.x, reinterpret_cast<int*>(sA0), sRows, sInfo,
@@ -441,7 +463,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const int KT = K / BK;
     const int KW = K >> 5;
     const float neg_alpha = -alpha_p[tenant];
+    const uint32_t neg_alpha_h = to_f16(neg_alpha) | ((uint32_t)to_f16(neg_alpha) << 16);
     packed += (size_t)tenant * N * KW;
+    // one pair of effective weights in one go (prologue)
+    auto fuse_full = [&](uint32_t wd, uint32_t sw_, int p) -> uint32_t {
+        if constexpr (ET == kF16) return fuse_pair_f16(wd, sw_, p, neg_alpha_h);
+        else return fuse_pair(wd, sw_, p, neg_alpha);
+    };
 
     // ---- staging assignment: per instruction i a wave moves rows
     //      32i + 8wv + (lane >> 3), lane l landing at LDS slot l & 7 ----
@@ -526,7 +554,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         const uint32_t sw0 = sign_word(s0[i]);
         u32x4 o;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w0[i][p], sw0, p, neg_alpha);
+        for (int p = 0; p < 4; ++p) o[p] = fuse_full(w0[i][p], sw0, p);
         *reinterpret_cast<u32x4*>(sB0 + i * 32 * BK + st_lane) = o;
     }
 #pragma unroll
@@ -537,7 +565,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         const uint32_t sw1 = sign_word(s1[i]);
         u32x4 o;
 #pragma unroll
-        for (int p = 0; p < 4; ++p) o[p] = fuse_pair(w1[i][p], sw1, p, neg_alpha);
+        for (int p = 0; p < 4; ++p) o[p] = fuse_full(w1[i][p], sw1, p);
         *reinterpret_cast<u32x4*>(sB1 + i * 32 * BK + st_lane) = o;
     }
 #pragma unroll
@@ -586,7 +614,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
 #pragma unroll
             for (int m = 0; m < 16; ++m) {
                 const int i = m >> 2, j = m & 3;
-                acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
+                acc[i][j] = mfma32<ET>(fb[j], fa[i], acc[i][j]);
                 if (m < 8) {
                     const uint16_t* abuf = b < 3 ? Ac : An;
                     const uint16_t* bbuf = b < 3 ? Bc : Bn;
@@ -605,8 +633,12 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                 uint16_t* const xdst = first ? An : Ac;
                 const int kr = first ? kr1 : kr2;
                 const int kx = first ? kx1 : kx2;
-                if ((u & 1) == 0) pw = fuse_pair_a(ws[c][u >> 1], sw, u >> 1);
-                else o[u >> 1] = fuse_pair_b(pw, neg_alpha);
+                if constexpr (ET == kF16) {
+                    if ((u & 1) == 0) o[u >> 1] = fuse_pair_f16(ws[c][u >> 1], sw, u >> 1, neg_alpha_h);
+                } else {
+                    if ((u & 1) == 0) pw = fuse_pair_a(ws[c][u >> 1], sw, u >> 1);
+                    else o[u >> 1] = fuse_pair_b(pw, neg_alpha);
+                }
                 if (u == 6) {
                     // sign word of the next chunk in stream order
                     sw_next = c < 7 ? sign_word(ss[c + 1]) : sign_word(sn2[0]);
@@ -638,7 +670,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     //      consecutive columns per register quad ----
     const int lrow = wm * 128 + (lane & 31);
     const int ncol = n0 + wn * 128 + 4 * (lane >> 5);
-    if constexpr (YDT == kBF16 && ALIGNED) {
+    if constexpr (YDT != kF32 && ALIGNED) {
         // Rows go through LDS, 64 at a time, so that each lane stores 16
         // contiguous bytes and a store instruction covers whole 256-byte rows.
         raw_barrier();  // every wave is done with the operand buffers
@@ -656,8 +688,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                         const f32x2v lo = {acc[i][j][4 * q], acc[i][j][4 * q + 1]};
                         const f32x2v hi = {acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
                         uint2 v;
-                        v.x = __builtin_bit_cast(uint32_t, __builtin_convertvector(lo, bf16x2v));
-                        v.y = __builtin_bit_cast(uint32_t, __builtin_convertvector(hi, bf16x2v));
+                        v.x = cvt_pair<ET>(lo);
+                        v.y = cvt_pair<ET>(hi);
                         *reinterpret_cast<uint2*>(stage + (32 * ii + (lane & 31)) * kStageRow + 32 * j +
                                                   8 * q + 4 * (lane >> 5)) = v;
                     }
@@ -697,7 +729,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                     }
                 }
     } else {
-        // bf16 rows not 16-byte aligned: element stores
+        // 16-bit rows not 16-byte aligned: element stores
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -708,7 +740,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                     const bool ok = out_row(lrow + 32 * i, row);
                     const int col = ncol + 32 * j + 8 * (r >> 2) + (r & 3);
                     if (ok && col < N)
-                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_bf16(acc[i][j][r]);
+                        reinterpret_cast<uint16_t*>(y)[(size_t)row * N + col] = to_half<ET>(acc[i][j][r]);
                 }
     }
 }
@@ -722,29 +754,49 @@ bool prefill_stream_supported(int M, int N, int K) {
            (int64_t)N * K < ((int64_t)1 << 30);
 }
 
+namespace {
+
+template <int ET, bool GROUPED>
+void launch_stream_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                      const uint32_t* packed, const float* alpha, const int32_t* ids, int T,
+                      void* y, int y_dtype, int tiles_m, int grid, int tiles_n,
+                      hipStream_t stream) {
+    const dim3 g(grid), block(kThreads);
+    if (y_dtype != kF32 && N % 8 == 0)
+        prefill_stream_kernel<ET, ET, true, GROUPED><<<g, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+    else if (y_dtype != kF32)
+        prefill_stream_kernel<ET, ET, false, GROUPED><<<g, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+    else if (N % 4 == 0)
+        prefill_stream_kernel<ET, kF32, true, GROUPED><<<g, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+    else
+        prefill_stream_kernel<ET, kF32, false, GROUPED><<<g, block, 0, stream>>>(
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+}
+
+}  // namespace
+
 hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                           const uint32_t* packed, const float* alpha, void* y, int y_dtype,
-                          hipStream_t stream) {
+                          int et, hipStream_t stream) {
     const int tiles_m = (M + BM - 1) / BM;
     const int tiles_n = (N + BN - 1) / BN;
-    const dim3 grid(tiles_m * tiles_n), block(kThreads);
-    const int32_t* no_ids = nullptr;
+    const int grid = tiles_m * tiles_n;
     if (prefill_stream_supported(M, N, K)) {
-        if (y_dtype == kBF16 && N % 8 == 0)
-            prefill_stream_kernel<kBF16, true, false><<<grid, block, 0, stream>>>(
-                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
-        else if (y_dtype == kBF16)
-            prefill_stream_kernel<kBF16, false, false><<<grid, block, 0, stream>>>(
-                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
-        else if (N % 4 == 0)
-            prefill_stream_kernel<kF32, true, false><<<grid, block, 0, stream>>>(
-                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+        if (et == kF16)
+            launch_stream_et<kF16, false>(x, M, K, w, N, packed, alpha, nullptr, 1, y, y_dtype,
+                                          tiles_m, grid, tiles_n, stream);
         else
-            prefill_stream_kernel<kF32, false, false><<<grid, block, 0, stream>>>(
-                x, M, K, w, N, packed, alpha, no_ids, 1, y, tiles_m, tiles_n);
+            launch_stream_et<kBF16, false>(x, M, K, w, N, packed, alpha, nullptr, 1, y, y_dtype,
+                                           tiles_m, grid, tiles_n, stream);
+    } else if (et == kF16) {
+        prefill_general_kernel<kF16><<<grid, kThreads, 0, stream>>>(x, M, K, w, N, packed, alpha, y,
+                                                                   y_dtype, tiles_m, tiles_n);
     } else {
-        prefill_general_kernel<<<grid, block, 0, stream>>>(x, M, K, w, N, packed, alpha, y, y_dtype,
-                                                         tiles_m, tiles_n);
+        prefill_general_kernel<kBF16><<<grid, kThreads, 0, stream>>>(x, M, K, w, N, packed, alpha, y,
+                                                                    y_dtype, tiles_m, tiles_n);
     }
     return hipGetLastError();
 }
@@ -756,25 +808,19 @@ bool prefill_grouped_supported(int M, int N, int K, int T) {
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,
                                   const int32_t* tenant_ids, int T, void* y, int y_dtype,
-                                  hipStream_t stream) {
+                                  int et, hipStream_t stream) {
     // sum_t ceil(c_t / BM) over the U <= min(T, M) tenants present, with
     // sum_t c_t <= M, is at most (M + (BM - 1) * U) / BM
     const int64_t U = T < M ? T : M;
     const int tiles_m = (int)(((int64_t)M + (BM - 1) * U) / BM);
     const int tiles_n = (N + BN - 1) / BN;
-    const dim3 grid((tiles_m + 1) * tiles_n), block(kThreads);
-    if (y_dtype == kBF16 && N % 8 == 0)
-        prefill_stream_kernel<kBF16, true, true><<<grid, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
-    else if (y_dtype == kBF16)
-        prefill_stream_kernel<kBF16, false, true><<<grid, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
-    else if (N % 4 == 0)
-        prefill_stream_kernel<kF32, true, true><<<grid, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
+    const int grid = (tiles_m + 1) * tiles_n;
+    if (et == kF16)
+        launch_stream_et<kF16, true>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype,
+                                     tiles_m, grid, tiles_n, stream);
     else
-        prefill_stream_kernel<kF32, false, true><<<grid, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, tenant_ids, T, y, tiles_m, tiles_n);
+        launch_stream_et<kBF16, true>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype,
+                                      tiles_m, grid, tiles_n, stream);
     return hipGetLastError();
 }
 

@@ -62,7 +62,7 @@ __device__ __forceinline__ void wave_range(int KB, int wv, int nw, int& kb0, int
 // never predicated: rows beyond M or N are clamped onto the last valid row
 // (they only feed output rows/columns that are not stored), which keeps the
 // loads free of branches and lets the compiler wait on the oldest stage only.
-template <int MB, int NW, int D>
+template <int ET, int MB, int NW, int D>
 __global__ __launch_bounds__(NW * 64) void skinny_single_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -105,11 +105,11 @@ __global__ __launch_bounds__(NW * 64) void skinny_single_kernel(
             __builtin_amdgcn_sched_barrier(0);
         };
         auto consume = [&](int slot) {
-            const u32x4 sf = decode_signs8(sb[slot]);
+            const u32x4 sf = decode_signs8<ET>(sb[slot]);
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) {
-                accb[mb] = mfma16(xf[slot][mb], wf[slot], accb[mb]);
-                accs[mb] = mfma16(xf[slot][mb], sf, accs[mb]);
+                accb[mb] = mfma16<ET>(xf[slot][mb], wf[slot], accb[mb]);
+                accs[mb] = mfma16<ET>(xf[slot][mb], sf, accs[mb]);
             }
         };
         // Rounds of D blocks: all D loads of a round are issued back to back
@@ -153,14 +153,11 @@ __global__ __launch_bounds__(NW * 64) void skinny_single_kernel(
             s += sh.red_sign[v][m][f];
         }
         const float out = __builtin_fmaf(a, s, b);
-        if (y_dtype == kF32)
-            reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
-        else
-            reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+        store_y<ET>(y, (size_t)m * N + nn, out, y_dtype);
     }
 }
 
-template <int MB, int NW, int U, int SBP>
+template <int ET, int MB, int NW, int U, int SBP>
 __global__ __launch_bounds__(NW * 64) void skinny_multi_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
@@ -264,13 +261,13 @@ __global__ __launch_bounds__(NW * 64) void skinny_multi_kernel(
             for (int u = 0; u < UU; ++u) {
                 if (do_base) {
 #pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) accb[mb] = mfma16(xf[u][mb], wf[u], accb[mb]);
+                    for (int mb = 0; mb < MB; ++mb) accb[mb] = mfma16<ET>(xf[u][mb], wf[u], accb[mb]);
                 }
 #pragma unroll
                 for (int b = 0; b < SBP; ++b) {
                     if (bact[b]) {
-                        const u32x4 sf = decode_signs8(sign_byte(sw[u][b], g));
-                        accs[b] = mfma16(gf[u][b], sf, accs[b]);
+                        const u32x4 sf = decode_signs8<ET>(sign_byte(sw[u][b], g));
+                        accs[b] = mfma16<ET>(gf[u][b], sf, accs[b]);
                     }
                 }
             }
@@ -314,60 +311,67 @@ __global__ __launch_bounds__(NW * 64) void skinny_multi_kernel(
             }
             out = __builtin_fmaf(alpha[t], s, b);
         }
-        if (y_dtype == kF32)
-            reinterpret_cast<float*>(y)[(size_t)m * N + nn] = out;
-        else
-            reinterpret_cast<uint16_t*>(y)[(size_t)m * N + nn] = to_bf16(out);
+        store_y<ET>(y, (size_t)m * N + nn, out, y_dtype);
     }
 }
 
 constexpr int kWaves = 8;
 
-template <int MB>
+template <int ET, int MB>
 hipError_t launch_single_mb(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                             const uint32_t* packed, const float* alpha, void* y, int y_dtype,
                             hipStream_t stream) {
     const int grid = (N + kFeat - 1) / kFeat;
     constexpr int D = MB == 1 ? 16 : (MB == 2 ? 12 : 8);
-    skinny_single_kernel<MB, kWaves, D><<<grid, kWaves * 64, 0, stream>>>(
+    skinny_single_kernel<ET, MB, kWaves, D><<<grid, kWaves * 64, 0, stream>>>(
         x, M, K, w, N, packed, alpha, y, y_dtype);
     return hipGetLastError();
 }
 
-template <int MB>
+template <int ET, int MB>
 hipError_t launch_multi_mb(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                            const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
                            int T, void* y, int y_dtype, hipStream_t stream) {
     const int grid = (N + kFeat - 1) / kFeat;
-    skinny_multi_kernel<MB, kWaves, 2, 8><<<grid, kWaves * 64, 0, stream>>>(
+    skinny_multi_kernel<ET, MB, kWaves, 2, 8><<<grid, kWaves * 64, 0, stream>>>(
         x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype);
     return hipGetLastError();
+}
+
+template <int ET>
+hipError_t launch_skinny_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                            const uint32_t* packed, const float* alpha,
+                            const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                            hipStream_t stream) {
+    const int mb = (M + 15) / 16;
+    if (tenant_ids == nullptr) {
+        if (M <= 16) return launch_decode(x, M, K, w, N, packed, alpha, y, y_dtype, ET, stream);
+        switch (mb) {
+            case 1: return launch_single_mb<ET, 1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+            case 2: return launch_single_mb<ET, 2>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+            case 3: return launch_single_mb<ET, 3>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+            default: return launch_single_mb<ET, 4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
+        }
+    }
+    if (multi_supported(K))
+        return launch_multi(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, ET, stream);
+    switch (mb) {
+        case 1: return launch_multi_mb<ET, 1>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        case 2: return launch_multi_mb<ET, 2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        case 3: return launch_multi_mb<ET, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        default: return launch_multi_mb<ET, 4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    }
 }
 
 }  // namespace
 
 hipError_t launch_skinny(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                          const uint32_t* packed, const float* alpha,
-                         const int32_t* tenant_ids, int T, void* y, int y_dtype,
+                         const int32_t* tenant_ids, int T, void* y, int y_dtype, int et,
                          hipStream_t stream) {
-    const int mb = (M + 15) / 16;
-    if (tenant_ids == nullptr) {
-        if (M <= 16) return launch_decode(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-        switch (mb) {
-            case 1: return launch_single_mb<1>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-            case 2: return launch_single_mb<2>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-            case 3: return launch_single_mb<3>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-            default: return launch_single_mb<4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
-        }
-    }
-    if (multi_supported(K))
-        return launch_multi(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-    switch (mb) {
-        case 1: return launch_multi_mb<1>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        case 2: return launch_multi_mb<2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        case 3: return launch_multi_mb<3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        default: return launch_multi_mb<4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-    }
+    if (et == kF16)
+        return launch_skinny_et<kF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    return launch_skinny_et<kBF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
 }
 
 }  // namespace bitdelta

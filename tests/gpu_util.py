@@ -22,6 +22,13 @@ def dev_bf16(bits: np.ndarray):
     return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(t.bfloat16).cuda()
 
 
+def dev_half(bits: np.ndarray, dtype: str):
+    """bf16 or fp16 bit patterns -> device tensor of that type."""
+    t = torch()
+    tt = t.float16 if dtype == "f16" else t.bfloat16
+    return t.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(tt).cuda()
+
+
 def dev_words(words: np.ndarray):
     t = torch()
     return t.from_numpy(np.ascontiguousarray(words).view(np.int32)).cuda()
@@ -42,11 +49,13 @@ def host_words(t_words) -> np.ndarray:
 
 
 def host_out(y) -> np.ndarray:
-    """Device output (fp32 or bf16) -> float64 host array."""
+    """Device output (fp32, bf16 or fp16) -> float64 host array."""
     t = torch()
     if y.dtype == t.bfloat16:
         bits = y.view(t.int16).cpu().numpy().view(np.uint16)
         return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    if y.dtype == t.float16:
+        return y.view(t.int16).cpu().numpy().view(np.float16).astype(np.float64)
     return y.cpu().numpy().astype(np.float64)
 
 
@@ -56,9 +65,10 @@ def run_matmul(p, packed=None, path=0, y_dtype=None):
     t = torch()
     packed = p.packed if packed is None else packed
     yd = y_dtype or p.y_dtype
-    out_dtype = t.float32 if yd == "f32" else t.bfloat16
+    dt = getattr(p, "dtype", "bf16")
+    out_dtype = t.float32 if yd == "f32" else (t.float16 if dt == "f16" else t.bfloat16)
     tid = None if p.tenant_ids is None else dev_i32(p.tenant_ids)
-    y = bd.matmul(dev_bf16(p.x), dev_bf16(p.w), dev_words(packed), dev_f32(p.alpha),
+    y = bd.matmul(dev_half(p.x, dt), dev_half(p.w, dt), dev_words(packed), dev_f32(p.alpha),
                   tenant_ids=tid, out_dtype=out_dtype, path=path)
     t.cuda.synchronize()
     return y

@@ -134,24 +134,41 @@ def test_pack_unpack_errors(lib):
 
 def test_compress_errors(lib):
     F, Bs, Pk, R, Al = A, B, C, D, E
-    cp = lib.bitdelta_compress
-    assert cp(F, Bs, 4, 48, Pk, R, Al, None) == -2        # K % 32
-    assert cp(F, Bs, -1, 32, Pk, R, Al, None) == -2
-    assert cp(F, Bs, 4, -32, Pk, R, Al, None) == -2
-    assert cp(None, Bs, 4, 32, Pk, R, Al, None) == -1
-    assert cp(F, None, 4, 32, Pk, R, Al, None) == -1
-    assert cp(F, Bs, 4, 32, None, R, Al, None) == -1
-    assert cp(F, Bs, 4, 32, Pk, None, Al, None) == -1      # row sums are required
-    assert cp(F + 8, Bs, 4, 32, Pk, R, Al, None) == -3
-    assert cp(F, Bs + 2, 4, 32, Pk, R, Al, None) == -3
-    assert cp(F, Bs, 4, 32, Pk + 2, R, Al, None) == -3
-    assert cp(F, Bs, 4, 32, Pk, R + 1, Al, None) == -3
-    assert cp(F, Bs, 4, 32, Pk, R, Al + 2, None) == -3
-    assert cp(F, Bs, 4, 32, F + 64, R, Al, None) == -7     # packed inside w_fine
-    assert cp(F, Bs, 4, 32, Pk, Pk, Al, None) == -7        # row sums over packed
-    assert cp(F, Bs, 4, 32, Pk, R, R, None) == -7          # alpha over row sums
-    assert cp(F, Bs, 0, 32, Pk, R, Al, None) == 0
-    assert cp(F, Bs, 4, 0, Pk, R, Al, None) == 0
+
+    def cp(f, b, rows, K, pk, r, al, dt=bd.BF16):
+        return lib.bitdelta_compress(f, b, rows, K, dt, pk, r, al, None)
+    assert cp(F, Bs, 4, 48, Pk, R, Al) == -2        # K % 32
+    assert cp(F, Bs, -1, 32, Pk, R, Al) == -2
+    assert cp(F, Bs, 4, -32, Pk, R, Al) == -2
+    assert cp(F, Bs, 4, 32, Pk, R, Al, dt=bd.F32) == -4
+    assert cp(F, Bs, 4, 32, Pk, R, Al, dt=bd.I8) == -4
+    assert cp(None, Bs, 4, 32, Pk, R, Al) == -1
+    assert cp(F, None, 4, 32, Pk, R, Al) == -1
+    assert cp(F, Bs, 4, 32, None, R, Al) == -1
+    assert cp(F, Bs, 4, 32, Pk, None, Al) == -1      # row sums are required
+    assert cp(F + 8, Bs, 4, 32, Pk, R, Al) == -3
+    assert cp(F, Bs + 2, 4, 32, Pk, R, Al) == -3
+    assert cp(F, Bs, 4, 32, Pk + 2, R, Al) == -3
+    assert cp(F, Bs, 4, 32, Pk, R + 1, Al) == -3
+    assert cp(F, Bs, 4, 32, Pk, R, Al + 2) == -3
+    assert cp(F, Bs, 4, 32, F + 64, R, Al) == -7     # packed inside w_fine
+    assert cp(F, Bs, 4, 32, Pk, Pk, Al) == -7        # row sums over packed
+    assert cp(F, Bs, 4, 32, Pk, R, R) == -7          # alpha over row sums
+    assert cp(F, Bs, 0, 32, Pk, R, Al) == 0
+    assert cp(F, Bs, 4, 0, Pk, R, Al, dt=bd.F16) == 0
+
+
+def test_typed_matmul_dtype_errors(lib):
+    def mt(in_dt, y_dt):
+        return lib.bitdelta_matmul_typed(A, 4, 64, B, 8, C, D, None, 1, in_dt, E, y_dt,
+                                         bd.PATH_AUTO, None)
+    assert mt(bd.F32, bd.F32) == -4          # inputs are 16-bit
+    assert mt(bd.I8, bd.F32) == -4
+    assert mt(bd.F16, bd.BF16) == -4         # a 16-bit output has the input type
+    assert mt(bd.BF16, bd.F16) == -4
+    assert mt(7, bd.F32) == -4
+    assert lib.bitdelta_matmul_typed(A, 0, 64, B, 8, C, D, None, 1, bd.F16, E, bd.F16,
+                                     bd.PATH_AUTO, None) == 0
 
 
 def test_path_selection(lib):

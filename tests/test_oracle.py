@@ -361,3 +361,52 @@ def test_compress_worked_rows_and_signed_zeros():
     assert [int(w) for w in packed[:, 0]] == [0x55555555, 0xFFFFFFFF, 0x80000000, 0xFFFFFFFE]
     assert list(row_abs) == [8.0, 0.0, 16.0, 0.0]
     assert alpha == 24.0 / (4 * K)
+
+
+# ---------------------------------------------------------------- fp16 inputs
+
+def test_f16_decode_every_finite_pattern():
+    # one-hot x picks W[n][0]; alpha = 0, so y[n] is the exact value of the
+    # fp16 pattern, compared with numpy's float16 -> float64 conversion
+    pats = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    finite = pats[((pats >> 10) & 0x1F) != 0x1F]
+    N, K = finite.size, 32
+    w = np.zeros((N, K), np.uint16)
+    w[:, 0] = finite
+    x = np.zeros((1, K), np.uint16)
+    x[0, 0] = 0x3C00  # 1.0
+    packed = np.zeros((1, N, 1), np.uint32)
+    y = oracle.matmul(x, w, packed, np.zeros(1, np.float32), dtype="f16")[0]
+    ref = finite.view(np.float16).astype(np.float64)
+    assert np.array_equal(y, ref)
+
+
+def test_brute_force_f16_decoder_matches_numpy():
+    pats = np.arange(0, 1 << 16, 7, dtype=np.uint32).astype(np.uint16)
+    pats = pats[((pats >> 10) & 0x1F) != 0x1F]
+    from fractions import Fraction
+    for h in pats:
+        assert brute.f16_bits_to_fraction(int(h)) == Fraction(float(np.uint16(h).view(np.float16)))
+
+
+@pytest.mark.parametrize("M,N,K,T", [(2, 3, 32, 1), (3, 2, 64, 2)])
+def test_brute_force_f16(M, N, K, T):
+    rng = np.random.default_rng(M * 10 + K)
+    p = wl.make_problem(M, N, K, T, seed=M + N + K, multi_tenant=T > 1, dtype="f16", y_dtype="f32")
+    exact = brute.matmul_exact(p.x, p.w, p.packed, p.alpha, p.tenant_ids, dtype="f16")
+    y = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids, dtype="f16")
+    for m in range(M):
+        for n in range(N):
+            e = float(exact[m][n])
+            assert abs(y[m, n] - e) <= 1e-15 * max(1.0, abs(e)), (m, n)
+
+
+def test_f16_compress_bits_equal_numpy_signbit():
+    rng = np.random.default_rng(34)
+    base = wl.normal_f16(rng, (20, 256), 0.02)
+    fine = wl.normal_f16(rng, (20, 256), 0.02)
+    fine[:, ::5] = base[:, ::5]
+    packed, row_abs, _ = oracle.compress(fine, base, dtype="f16")
+    d = base.view(np.float16).astype(np.float64)
+    d = fine.view(np.float16).astype(np.float64) - d
+    np.testing.assert_array_equal(packed, numpy_pack(~np.signbit(d)))

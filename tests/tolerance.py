@@ -22,8 +22,14 @@ def bf16_to_f64(bits):
     return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
+def half_to_f64(bits, dtype="bf16"):
+    if dtype == "f16":
+        return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(np.float64)
+    return bf16_to_f64(bits)
+
+
 def check(y, y_ref, x_bits, w_bits, alpha, tenant_ids=None, rows=None,
-          rel_frob=REL_FROB, elem_factor=ELEM_FACTOR):
+          rel_frob=REL_FROB, elem_factor=ELEM_FACTOR, dtype="bf16"):
     """Raise AssertionError with a diagnostic when y misses either bar.
 
     y, y_ref: float arrays [M', C] (C sampled columns); rows: the x rows they
@@ -34,12 +40,12 @@ def check(y, y_ref, x_bits, w_bits, alpha, tenant_ids=None, rows=None,
     assert y.shape == y_ref.shape, (y.shape, y_ref.shape)
     assert np.all(np.isfinite(y_ref)), "reference has non-finite entries"
     assert np.all(np.isfinite(y)), f"result has {np.count_nonzero(~np.isfinite(y))} non-finite entries"
-    x = bf16_to_f64(x_bits)
+    x = half_to_f64(x_bits, dtype)
     if rows is not None:
         x = x[np.asarray(rows)]
     alpha = np.atleast_1d(np.asarray(alpha, dtype=np.float64))
     used = alpha if tenant_ids is None else alpha[np.unique(np.asarray(tenant_ids))]
-    wmax = float(np.max(np.abs(bf16_to_f64(w_bits)))) + float(np.max(np.abs(used)))
+    wmax = float(np.max(np.abs(half_to_f64(w_bits, dtype)))) + float(np.max(np.abs(used)))
     num = np.linalg.norm(y - y_ref)
     den = np.linalg.norm(y_ref)
     relf = num / den if den > 0 else num

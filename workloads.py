@@ -20,7 +20,8 @@ workloads below are LLaMA-7B-shaped stand-ins:
 Distributions: x ~ N(0, 1); W ~ N(0, 0.02) (0.02 is the standard deviation);
 sign bits i.i.d. Bernoulli(0.5); alpha ~ U(1e-4, 1e-3) per tenant (and per
 matrix in the sweep); tenant ids uniform over [0, T).  Normal draws are made in
-float32 and rounded to bfloat16 with round-to-nearest-even.  Draw order inside
+float32 and rounded to bfloat16 (or, for the fp16 variants of the same shapes,
+to IEEE fp16) with round-to-nearest-even.  Draw order inside
 one generator: x, W, signs, alpha, tenant ids.
 
 The tiny workload draws its signs as int8 +1/-1 (so that the packer is
@@ -58,7 +59,8 @@ class Problem:
     packed: Optional[np.ndarray] = None   # uint32 [T, N, K/32]
     signs: Optional[np.ndarray] = None    # int8 [T, N, K] (+1/-1), tiny only
     tenant_ids: Optional[np.ndarray] = None  # int32 [M] or None
-    y_dtype: str = "bf16"
+    y_dtype: str = "bf16"            # "f32" or the input type
+    dtype: str = "bf16"              # 16-bit type of x and W: "bf16" or "f16"
     meta: dict = field(default_factory=dict)
 
     @property
@@ -94,6 +96,18 @@ def normal_bf16(rng: np.random.Generator, shape, std: float) -> np.ndarray:
     return f32_to_bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(std))
 
 
+def normal_f16(rng: np.random.Generator, shape, std: float) -> np.ndarray:
+    """fp32 normal draws rounded to IEEE fp16 (nearest even), as bit patterns."""
+    return (rng.standard_normal(shape, dtype=np.float32) * np.float32(std)).astype(np.float16).view(np.uint16)
+
+
+def half_bits_to_f32(h: np.ndarray, dtype: str) -> np.ndarray:
+    """bf16 or fp16 bit patterns -> float32 values (exact)."""
+    if dtype == "f16":
+        return np.asarray(h, dtype=np.uint16).view(np.float16).astype(np.float32)
+    return bf16_bits_to_f32(h)
+
+
 def uniform_words(rng: np.random.Generator, shape) -> np.ndarray:
     return rng.integers(0, 2**32, size=shape, dtype=np.uint64).astype(np.uint32)
 
@@ -123,11 +137,14 @@ def prompt_tenant_ids(rng: np.random.Generator, M: int, T: int, prompts: int) ->
 def make_problem(M: int, N: int, K: int, T: int = 1, *, seed: int = 0,
                  multi_tenant: bool = False, y_dtype: str = "bf16",
                  x_std: float = 1.0, w_std: float = 0.02,
-                 signs_as_int8: bool = False, name: str = "custom") -> Problem:
-    """Generic generator: x ~ N(0, x_std), W ~ N(0, w_std), Bernoulli signs."""
+                 signs_as_int8: bool = False, name: str = "custom",
+                 dtype: str = "bf16") -> Problem:
+    """Generic generator: x ~ N(0, x_std), W ~ N(0, w_std), Bernoulli signs.
+    dtype picks the 16-bit type of x and W; y_dtype "half" means that type."""
     rng = np.random.default_rng(seed)
-    x = normal_bf16(rng, (M, K), x_std)
-    w = normal_bf16(rng, (N, K), w_std)
+    normal = normal_f16 if dtype == "f16" else normal_bf16
+    x = normal(rng, (M, K), x_std)
+    w = normal(rng, (N, K), w_std)
     packed = signs = None
     if signs_as_int8:
         signs = random_signs_i8(rng, (T, N, K))
@@ -135,8 +152,10 @@ def make_problem(M: int, N: int, K: int, T: int = 1, *, seed: int = 0,
         packed = uniform_words(rng, (T, N, K // 32))
     a = alphas(rng, T)
     tid = tenant_draw(rng, M, T) if multi_tenant else None
+    if y_dtype == "half":
+        y_dtype = dtype
     return Problem(name, x, w, a, packed=packed, signs=signs, tenant_ids=tid,
-                   y_dtype=y_dtype)
+                   y_dtype=y_dtype, dtype=dtype)
 
 
 def tiny(seed: int = 0) -> Problem:
@@ -144,8 +163,9 @@ def tiny(seed: int = 0) -> Problem:
                         name="tiny 4x256 . 512x256, fp32 out")
 
 
-def decode(M: int, seed: int = 0) -> Problem:
-    return make_problem(M, 4096, 4096, 1, seed=seed, name=f"decode M={M} 4096x4096")
+def decode(M: int, seed: int = 0, dtype: str = "bf16") -> Problem:
+    return make_problem(M, 4096, 4096, 1, seed=seed, name=f"decode M={M} 4096x4096 {dtype}",
+                        dtype=dtype, y_dtype=dtype)
 
 
 def mt_decode(seed: int = 0) -> Problem:
@@ -153,8 +173,9 @@ def mt_decode(seed: int = 0) -> Problem:
                         name="multi-tenant decode M=32 11008x4096 T=16")
 
 
-def prefill(seed: int = 0) -> Problem:
-    return make_problem(4096, 4096, 4096, 1, seed=seed, name="prefill 4096^3")
+def prefill(seed: int = 0, dtype: str = "bf16") -> Problem:
+    return make_problem(4096, 4096, 4096, 1, seed=seed, name=f"prefill 4096^3 {dtype}",
+                        dtype=dtype, y_dtype=dtype)
 
 
 MT_PREFILL = {"M": 4096, "N": 4096, "K": 4096, "T": 8, "prompts": 16}
@@ -200,20 +221,20 @@ def llama_matrix(layer: int, idx: int, shared=None, seed: int = 0) -> Problem:
 # ---- device-side generation for the benchmark (same recipe, torch RNG) ----
 
 def device_problem(M: int, N: int, K: int, T: int, *, multi_tenant: bool, seed: int,
-                   device="cuda", x_std: float = 1.0, w_std: float = 0.02, prompts: int = 0):
+                   device="cuda", x_std: float = 1.0, w_std: float = 0.02, prompts: int = 0,
+                   dtype: str = "bf16"):
     """Same distributions, drawn directly into device memory with torch's RNG.
 
-    Returns a dict of torch tensors: x (bf16 [M,K]), w (bf16 [N,K]),
+    Returns a dict of torch tensors: x (bf16 or fp16 [M,K]), w (same, [N,K]),
     packed (int32 [T,N,K/32]), alpha (fp32 [T]), tenant_ids (int32 [M] or None).
     With prompts > 0 the tenant ids follow prompt_tenant_ids (drawn on the host).
     """
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(seed)
-    x = (torch.randn((M, K), generator=g, device=device, dtype=torch.float32) * x_std
-         ).to(torch.bfloat16)
-    w = (torch.randn((N, K), generator=g, device=device, dtype=torch.float32) * w_std
-         ).to(torch.bfloat16)
+    half = torch.float16 if dtype == "f16" else torch.bfloat16
+    x = (torch.randn((M, K), generator=g, device=device, dtype=torch.float32) * x_std).to(half)
+    w = (torch.randn((N, K), generator=g, device=device, dtype=torch.float32) * w_std).to(half)
     packed = torch.randint(0, 256, (T, N, K // 32, 4), generator=g, device=device,
                            dtype=torch.uint8).view(torch.int32).reshape(T, N, K // 32)
     alpha = (torch.rand((T,), generator=g, device=device, dtype=torch.float32)
