@@ -33,6 +33,7 @@ if ROOT not in sys.path:
 METRIC = "binary-delta matmul TB/s (decode) & TFLOP/s (prefill), % of MI355X roofline"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 matrix peak, published
+F16_PEAK_TFLOPS = 2500.0       # MI355X dense fp16 matrix peak, published
 MALL_BYTES = 256 << 20
 
 
@@ -55,9 +56,10 @@ class Launcher:
         M, K = x.shape
         N = w.shape[0]
         T = alpha.numel()
+        dt = bd.F16 if x.dtype == torch.float16 else bd.BF16
         args = (x.data_ptr(), M, K, w.data_ptr(), N, packed.data_ptr(), alpha.data_ptr(),
-                None if tid is None else tid.data_ptr(), T, y.data_ptr(), bd.BF16, bd.PATH_AUTO)
-        f = self.lib.bitdelta_matmul_with_path
+                None if tid is None else tid.data_ptr(), T, dt, y.data_ptr(), dt, bd.PATH_AUTO)
+        f = self.lib.bitdelta_matmul_typed
 
         def call():
             rc = f(*args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
@@ -66,12 +68,12 @@ class Launcher:
         return call
 
 
-def make_sets(count, M, N, K, T, multi, seed, dev, prompts=0):
+def make_sets(count, M, N, K, T, multi, seed, dev, prompts=0, dtype="bf16"):
     import workloads as wl
     sets = []
     for i in range(count):
         d = wl.device_problem(M, N, K, T, multi_tenant=multi, seed=seed + i, device=dev,
-                              prompts=prompts)
+                              prompts=prompts, dtype=dtype)
         sets.append(d)
     return sets
 
@@ -118,7 +120,7 @@ def timed(replay, reps):
 
 
 def bench_workload(name, shapes, T, multi, flops_fn, steps, warmup, dev, launcher, seed,
-                   rotate=True, prompts=0):
+                   rotate=True, prompts=0, dtype="bf16"):
     """Time exactly `steps` steps; a step is one launch per (M, N, K) in `shapes`.
 
     With rotate, consecutive launches read different buffer sets and the sets
@@ -133,8 +135,8 @@ def bench_workload(name, shapes, T, multi, flops_fn, steps, warmup, dev, launche
     for r in range(nrot):
         step_calls, b = [], 0
         for j, (M, N, K) in enumerate(shapes):
-            d = make_sets(1, M, N, K, T, multi, seed + 1000 * j + r, dev, prompts)[0]
-            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            d = make_sets(1, M, N, K, T, multi, seed + 1000 * j + r, dev, prompts, dtype)[0]
+            y = torch.empty((M, N), dtype=d["x"].dtype, device=dev)
             used = 1 if d["tenant_ids"] is None else len(np.unique(d["tenant_ids"].cpu().numpy()))
             b += algorithmic_bytes(M, N, K, used)
             keep.append((d, y))
@@ -215,6 +217,7 @@ def bench_compress(dev, lib, steps, warmup):
     more than twice the Infinity Cache.  HBM-bound: 4 bytes read per weight."""
     import ctypes
     import torch
+    import paper_2609_36800_amd as bd
     rows, K = 11008, 4096
     per = rows * K * 4 + rows * K // 8 + rows * 4 + 4
     nsets = max(2, -(-2 * MALL_BYTES // per))
@@ -232,8 +235,8 @@ def bench_compress(dev, lib, steps, warmup):
 
     def call_for(st):
         fine, base, packed, row_abs, alpha = st
-        args = (fine.data_ptr(), base.data_ptr(), rows, K, packed.data_ptr(), row_abs.data_ptr(),
-                alpha.data_ptr())
+        args = (fine.data_ptr(), base.data_ptr(), rows, K, bd.BF16, packed.data_ptr(),
+                row_abs.data_ptr(), alpha.data_ptr())
 
         def c():
             rc = f(*args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
@@ -454,6 +457,17 @@ def main():
             20, args.warmup, dev, launcher, seed=130, rotate=False, prompts=c["prompts"])
         mpf["mfma_frac"] = mpf["TFLOPs"] / BF16_PEAK_TFLOPS
         workloads.append(mpf)
+        # the paper's own precision: the same decode pair and prefill with fp16 x and W
+        workloads.append(bench_workload(
+            "fp16 decode GEMV pair: x 1x4096 and 16x4096, W_base 4096x4096 (fp16), fp16 out",
+            [(1, 4096, 4096), (16, 4096, 4096)], 1, False, lambda M, N, K: 2 * M * N * K,
+            args.steps, args.warmup, dev, launcher, seed=301, dtype="f16"))
+        pf16 = bench_workload(
+            "fp16 prefill: x 4096x4096, W_base 4096x4096 (fp16), one tenant, fused fp16 GEMM",
+            [(4096, 4096, 4096)], 1, False, lambda M, N, K: 2 * M * N * K,
+            20, args.warmup, dev, launcher, seed=390, rotate=False, dtype="f16")
+        pf16["mfma_frac"] = pf16["TFLOPs"] / F16_PEAK_TFLOPS
+        workloads.append(pf16)
         workloads.append(llama_sweep(dev, launcher, args.warmup))
         workloads.append(bench_compress(dev, launcher.lib, 50, args.warmup))
 
