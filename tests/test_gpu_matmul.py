@@ -80,8 +80,9 @@ def test_prefill_workload_sampled():
     check(yh, ref, p.x, p.w, p.alpha, rows=rows)
 
 
-@pytest.mark.parametrize("layer", [0, 31])
+@pytest.mark.parametrize("layer", list(range(32)))
 def test_llama_sweep_layer_sampled(layer):
+    # every matrix of the 32-layer sweep, each checked on its own
     shared = wl.llama_shared_inputs(seed=0)
     rng = np.random.default_rng(layer)
     for idx in range(len(wl.LLAMA_MATRICES)):
@@ -227,7 +228,7 @@ def test_sign_only_random_x(path):
     assert rel < (1e-5 if path == SKINNY else 2.0 ** -8), rel
 
 
-@pytest.mark.parametrize("a", [0.0, -3e-4, 0.25])
+@pytest.mark.parametrize("a", [0.0, -3e-4, 0.25, 100.0])
 def test_alpha_values(a):
     for M, path in ((16, SKINNY), (96, PREFILL)):
         p = wl.make_problem(M, 130, 256, 1, seed=10, y_dtype="f32")
@@ -274,6 +275,37 @@ def test_extreme_magnitudes(path, x_std):
     log(f"extreme magnitudes x_std={x_std} path={path}")
     y = host_out(run_matmul(p, path=path))
     check(y, oracle_y(p), p.x, p.w, p.alpha)
+
+
+@pytest.mark.parametrize("path", [SKINNY, PREFILL])
+def test_overflow_to_inf(path):
+    # x near the top of the bf16 range against same-signed weights: every
+    # product has the row's sign, the exact sums exceed the fp32 range, and the
+    # outputs must be infinities of that sign; other rows stay finite
+    M = 8 if path == SKINNY else 80
+    N, K = 48, 256
+    p = wl.make_problem(M, N, K, 1, seed=17, y_dtype="f32")
+    big = wl.f32_to_bf16_bits(np.float32(3.0e38))
+    x = p.x.copy()
+    x[0, :] = big
+    x[1, :] = big ^ 0x8000
+    w = p.w.copy()
+    w[:16, :] = 0x3F80          # +1
+    w[16:32, :] = 0xBF80        # -1
+    # signs agree with the weights, so the separate base and sign sums of the
+    # decode path overflow with the same sign (no inf - inf)
+    pk = p.packed.copy()
+    pk[0, :16, :] = 0xFFFFFFFF
+    pk[0, 16:32, :] = 0
+    p.x, p.w, p.packed = x, w, pk
+    p.alpha = np.array([1e-3], np.float32)
+    log(f"overflow to inf path={path}")
+    y = host_out(run_matmul(p, path=path))
+    assert np.all(y[0, :16] == np.inf) and np.all(y[0, 16:32] == -np.inf)
+    assert np.all(y[1, :16] == -np.inf) and np.all(y[1, 16:32] == np.inf)
+    assert np.all(np.isfinite(y[2:]))
+    ref = oracle_y(p, rows=np.arange(2, M))
+    check(y[2:], ref, p.x, p.w, p.alpha, rows=np.arange(2, M))
 
 
 def test_cancellation_rows():
