@@ -304,14 +304,38 @@ def recorded_traffic():
     return rec.get("hbm_bytes_per_launch")
 
 
-def pmc_pass(steps):
-    """Launches for counter collection: the headline pair on rotating buffer
-    sets, then a plain device copy of 512 MiB whose FETCH_SIZE / WRITE_SIZE
-    readings calibrate the counters (known bytes read and written)."""
+def pmc_pass(steps, workload="decode"):
+    """Launches for counter collection.  decode: the headline pair on rotating
+    buffer sets, then a plain device copy of 512 MiB whose FETCH_SIZE /
+    WRITE_SIZE readings calibrate the counters (known bytes read and written).
+    prefill: `steps` launches each of the bf16 and fp16 4096^3 fused GEMM.
+    multi: `steps` launches of the batched kernel at 64 rows, 8 tenants,
+    4096x4096, on 12 rotating buffer sets."""
     import torch
     import paper_2609_36800_amd as bd
     dev = torch.device("cuda:0")
     launcher = Launcher(bd.load_library())
+    if workload in ("prefill", "multi"):
+        calls, keep = [], []
+        if workload == "prefill":
+            for dt in ("bf16", "f16"):
+                d = make_sets(1, 4096, 4096, 4096, 1, False, 3, dev, dtype=dt)[0]
+                y = torch.empty((4096, 4096), dtype=d["x"].dtype, device=dev)
+                keep.append((d, y))
+                calls += [launcher.matmul(d["x"], d["w"], d["packed"], d["alpha"], None, y)] * steps
+        else:
+            for r in range(12):
+                d = make_sets(1, 64, 4096, 4096, 8, True, 5 + r, dev)[0]
+                y = torch.empty((64, 4096), dtype=torch.bfloat16, device=dev)
+                keep.append((d, y))
+                calls.append(launcher.matmul(d["x"], d["w"], d["packed"], d["alpha"],
+                                             d["tenant_ids"], y))
+            calls = [calls[i % len(calls)] for i in range(steps)]
+        for c in calls:
+            c()
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_pass": workload, "launches": len(calls)}), flush=True)
+        return
     calls = []
     keep = []
     for r in range(8):
@@ -395,6 +419,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only launch the headline kernels and a calibration copy (for rocprofv3 --pmc)")
+    ap.add_argument("--pmc-workload", choices=("decode", "prefill", "multi"), default="decode",
+                    help="what --pmc-pass launches")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic record from two --pmc runs of --pmc-pass (no GPU needed)")
     args = ap.parse_args()
@@ -411,7 +437,7 @@ def main():
         sys.exit(2)
 
     if args.pmc_pass:
-        pmc_pass(args.steps)
+        pmc_pass(args.steps, args.pmc_workload)
         return
 
     import torch
