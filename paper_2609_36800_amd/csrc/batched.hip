@@ -1,0 +1,389 @@
+// Batched (multi-tenant) binary-delta matmul for at most 64 token rows with at
+// most 16 distinct tenants per call, K a multiple of 256:
+//
+//   y[m][n] = sum_k x[m][k] W[n][k] + alpha[t(m)] * sum_k x[m][k] s_t(m)[n][k]
+//
+// (the batched BitDelta GEMM of Section 4.4 at decode shapes).
+//
+// Cost model.  Every byte of W and the sign bits of each tenant present are
+// read once from HBM; x (a few hundred KB) is re-read from L2 by every
+// workgroup.  Turning one byte of sign bits into the eight bf16 +-1 values of
+// an MFMA operand takes nine VALU instructions, against 16 cycles for the
+// v_mfma_f32_16x16x32 that consumes them, so each tenant's signs are decoded
+// once per (16 features, 32-k block) and drive one product over all of that
+// tenant's rows.
+//
+// Routing.  The rows of each tenant are gathered into fragments of up to 16
+// rows (F fragments in all, a tenant with more rows gets more).  Per 32-k
+// block a fragment costs one x fragment read, one sign decode and two MFMAs
+// (x*W^T and x*S_t^T on the gathered rows).  F is known only on the device:
+// every workgroup computes the routing (wave 0, ballots) and enters the loop
+// specialised for its F.
+//
+// Memory path.  A 512-thread workgroup owns 16 output features; K runs in
+// 256-k tiles and wave w computes k-block w of every tile.  All operands reach
+// LDS by global->LDS copies of long row segments (a full cache line or more
+// per row), in three rings:
+//   W      16 rows x 512 B per tile, NWR slots, issued NWR-1 tiles ahead;
+//   x      XR rows x 512 B per tile, NXR slots, issued NXR-1 tiles ahead;
+//   signs  UMAX tenant slots x 16 rows x 128 B per 1024-k super-tile (four
+//          tiles), 2 slots.  The next super-tile is copied in two halves
+//          during the first two tiles of the current one (its slot was last
+//          read by the previous super-tile), and the last two tiles repeat
+//          the second half, so every tile issues the same copies.
+// Each tile's issue group is [sign part, x, W]: loads retire in issue order,
+// so one s_waitcnt vmcnt for the x of the tile about to be computed also
+// covers every earlier sign part while the deeper W ring stays in flight, and
+// one barrier per tile publishes the tile.
+//
+// The 8 waves' partial sums are added in a fixed order through LDS, so the
+// result is bitwise deterministic.
+#include <utility>
+
+#include "device.h"
+#include "internal.h"
+#include "ldscopy.h"
+
+namespace bitdelta {
+namespace {
+
+constexpr int kFeat = 16;
+constexpr int kWaves = 8;
+constexpr int kRowsMax = 64;
+constexpr int kTileK = 256;                    // k per tile (one 32-k block per wave)
+constexpr int kRowBytes = kTileK * 2;          // 512 B of one row per tile
+constexpr int kSuperTiles = 4;                 // tiles per sign super-tile
+constexpr int kSignRowBytes = kSuperTiles * kTileK / 8;   // 128 B of sign bits per row
+
+// Calls f(integral_constant<int, i>) for i = 0 .. N-1.
+template <typename Fn, int... Is>
+__device__ __forceinline__ void static_for_impl(Fn&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+__device__ __forceinline__ int swz16(int row, int chunk) { return chunk ^ (row & 15); }
+__device__ __forceinline__ int swz8(int row, int chunk) { return chunk ^ (row & 7); }
+
+struct Routing {
+    int tenant_of_row[kRowsMax];          // -1: id out of range
+    int frag_of_row[kRowsMax];            // fragment holding row m, -1: none
+    int frag_row[kRowsMax][16];           // row in slot i of fragment f, -1: empty
+    int frag_slot[kRowsMax];              // sign slot (distinct-tenant index) of fragment f
+    int slot_tenant[16];                  // tenant of sign slot u
+    uint32_t key_sorted[kRowsMax];
+    int sorted_row[kRowsMax];
+    int nfrag, nslot;
+};
+
+template <int XR, int UMAX, int NWR, int NXR>
+struct BatchedLayout {
+    static constexpr int kW = kFeat * kRowBytes;                  // 8 KB per W slot
+    static constexpr int kX = XR * kRowBytes;                     // per x slot
+    static constexpr int kS = UMAX * kFeat * kSignRowBytes;       // per sign slot
+    static constexpr int kWOff = 0;
+    static constexpr int kXOff = NWR * kW;
+    static constexpr int kSOff = kXOff + NXR * kX;
+    static constexpr int kRouteOff = kSOff + 2 * kS;
+    static constexpr int kTotal = kRouteOff + (int)sizeof(Routing);
+    // per-wave partials [wave][row][feature], base then sign, reuse the W and x rings
+    static constexpr int kRed = kWaves * kRowsMax * kFeat * 4;
+    static_assert(2 * kRed <= kSOff, "reduction area must fit in the W and x rings");
+    static_assert(kTotal <= 160 * 1024, "LDS budget");
+    // copies per wave per tile: sign part, x, W
+    static constexpr int kXOps = XR / 16;
+    static constexpr int kSOps = UMAX / 8;                        // half a super-tile: UMAX copies
+    static_assert(UMAX == 8 || UMAX == 16, "sign slots");
+    static_assert(NXR >= 2 && NWR >= NXR, "ring depths");
+};
+
+template <int ET, int XR, int UMAX, int NWR, int NXR, int F>
+__device__ __forceinline__ void batched_loop(char* lds, const Routing& rt, const uint16_t* __restrict__ x,
+                                             int M, int K, const uint16_t* __restrict__ w, int N,
+                                             const uint32_t* __restrict__ packed, int n0, int lane, int wv,
+                                             int f0) {
+    using L = BatchedLayout<XR, UMAX, NWR, NXR>;
+    const int li = lane & 15, g = lane >> 4;
+    const int KW = K >> 5, KT = K / kTileK;
+    const int NS = (KT + kSuperTiles - 1) / kSuperTiles;
+
+    // ---- copy sources (all clamped in range; surplus rows feed unstored outputs) ----
+    // W: wave w copies rows 2w, 2w+1 (lane >> 5), 16-byte chunk (lane & 31) swizzled
+    const int wrow = 2 * wv + (lane >> 5);
+    const uint16_t* wsrc = w + (size_t)min(n0 + wrow, N - 1) * K + 8 * swz16(wrow, lane & 31);
+    // x: wave w copies rows 2(w*XOPS + i) + (lane >> 5)
+    const uint16_t* xsrc[L::kXOps];
+#pragma unroll
+    for (int i = 0; i < L::kXOps; ++i) {
+        const int r = 2 * (wv * L::kXOps + i) + (lane >> 5);
+        xsrc[i] = x + (size_t)min(r, M - 1) * K + 8 * swz16(r, lane & 31);
+    }
+    // signs: the UMAX*16 (slot, feature) rows of a super-tile, 8 per copy with 8
+    // lanes per row; half h holds rows [h*UMAX*8, (h+1)*UMAX*8), copy j of wave w
+    // its rows 8*(w*kSOps + j) .. +7
+    int srow[2][L::kSOps];
+    const uint32_t* ssrc[2][L::kSOps];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < L::kSOps; ++j) {
+            srow[h][j] = h * UMAX * 8 + 8 * (wv * L::kSOps + j) + (lane >> 3);
+            const int u = srow[h][j] >> 4, f = srow[h][j] & 15;
+            const int t = rt.slot_tenant[min(u, rt.nslot - 1)];
+            ssrc[h][j] = packed + ((size_t)t * N + min(n0 + f, N - 1)) * KW;
+        }
+    const int schunk = lane & 7;
+
+    auto issue_x = [&](int tt) {
+        const int tc = min(tt, KT - 1);
+        char* buf = lds + L::kXOff + (tt % NXR) * L::kX;
+#pragma unroll
+        for (int i = 0; i < L::kXOps; ++i)
+            copy16_to_lds(xsrc[i] + (size_t)tc * kTileK, buf + (wv * L::kXOps + i) * 1024);
+    };
+    auto issue_w = [&](int tt) {
+        const int tc = min(tt, KT - 1);
+        copy16_to_lds(wsrc + (size_t)tc * kTileK, lds + L::kWOff + (tt % NWR) * L::kW + wv * 1024);
+    };
+    // half h of super-tile s
+    auto issue_s = [&](int s, int h) {
+        const int sc = min(s, NS - 1);
+#pragma unroll
+        for (int j = 0; j < L::kSOps; ++j) {
+            const int c = swz8(srow[h][j], schunk);                // source chunk at this position
+            const int word = min(32 * sc + 4 * c, KW - 4);
+            const int drow = h * UMAX * 8 + 8 * (wv * L::kSOps + j);     // first row of this copy
+            copy16_to_lds(ssrc[h][j] + word, lds + L::kSOff + (s & 1) * L::kS + drow * kSignRowBytes);
+        }
+    };
+
+    // ---- fragment read offsets ----
+    const int wchunk = 4 * wv + g;                                  // this lane's chunk of a tile row
+    const int woff = li * kRowBytes + 16 * swz16(li, wchunk);
+    // sign rows are (slot * 16 + feature): the swizzle key (row & 7) is li & 7 for
+    // every slot, and a fragment's slot only moves the row base (wave-uniform)
+    int xoff[F];
+    uint32_t sslot[F];
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+        int r = rt.frag_row[f0 + f][li];
+        if (r < 0) r = rt.frag_row[f0 + f][0];
+        xoff[f] = r * kRowBytes + 16 * swz16(r, wchunk);
+        sslot[f] = __builtin_amdgcn_readfirstlane((uint32_t)rt.frag_slot[f0 + f] * (kFeat * kSignRowBytes));
+    }
+    const int slane = li * kSignRowBytes + g + 4 * (wv & 3);       // + chunk per tile
+    f32x4 accb[F], accs[F];
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+        accb[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+        accs[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    // ---- prologue: super-tile 0, then the issue groups of tiles 0 .. NXR-2 / NWR-2 ----
+    constexpr int DX = NXR - 1, DW = NWR - 1;
+    issue_s(0, 0);
+    issue_s(0, 1);
+#pragma unroll
+    for (int i = 0; i < DW; ++i) {
+        if (i < DX) issue_x(i);
+        issue_w(i);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    // vmcnt after which the x of tile t (and so every sign part before it) and
+    // the W of tile t have landed: the copies issued later are the W of the
+    // group that issued x(t) (unless that group issued W(t) itself) and the DX-1
+    // whole groups after it
+    constexpr int kGroup = L::kSOps + L::kXOps + 1;
+    constexpr int kWait = (DW > DX ? 1 : 0) + (DX - 1) * kGroup;
+    for (int t = 0; t < KT; ++t) {
+        if (t == 0) wait_vm_lgkm0<0>();
+        else wait_vm_lgkm0<kWait>();
+        raw_barrier();
+        // issue group: sign half (t&3 < 2 ? t&3 : 1) of super-tile t/4+1, x(t+DX), W(t+DW)
+        issue_s((t >> 2) + 1, min(t & 3, 1));
+        issue_x(t + DX);
+        issue_w(t + DW);
+        __builtin_amdgcn_sched_barrier(0);
+
+        const int kb = t * 8 + wv;
+        if (kb < (K >> 5)) {
+            const char* wbuf = lds + L::kWOff + (t % NWR) * L::kW;
+            const char* xbuf = lds + L::kXOff + (t % NXR) * L::kX;
+            const char* sbuf = lds + L::kSOff + ((t >> 2) & 1) * L::kS;
+            // this wave's word of the tile is word 8*(t&3) + wv of the super-tile row:
+            // chunk 2*(t&3) + wv/4, stored at chunk ^ (row & 7)
+            const char* srd = sbuf + slane + 16 * (((2 * (t & 3)) + (wv >> 2)) ^ (li & 7));
+            const u32x4 bw = *reinterpret_cast<const u32x4*>(wbuf + woff);
+            // all of the tile's LDS reads first, so their latencies overlap
+            uint32_t sb[F];
+            u32x4 xa[F];
+#pragma unroll
+            for (int f = 0; f < F; ++f) {
+                sb[f] = *reinterpret_cast<const uint8_t*>(srd + sslot[f]);
+                xa[f] = *reinterpret_cast<const u32x4*>(xbuf + xoff[f]);
+            }
+#pragma unroll
+            for (int f = 0; f < F; ++f) {
+                accb[f] = mfma16<ET>(xa[f], bw, accb[f]);
+                accs[f] = mfma16<ET>(xa[f], decode_signs8<ET>(sb[f]), accs[f]);
+            }
+        }
+    }
+    // drain the copies of the tail tiles, then the rings become the reduction area
+    wait_vm_lgkm0<0>();
+    __syncthreads();
+    float* red_b = reinterpret_cast<float*>(lds);                  // [wave][row][feature]
+    float* red_s = red_b + kWaves * kRowsMax * kFeat;
+#pragma unroll
+    for (int f = 0; f < F; ++f)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int row = rt.frag_row[f0 + f][4 * g + r];
+            if (row >= 0) {
+                red_b[(wv * kRowsMax + row) * kFeat + li] = accb[f][r];
+                red_s[(wv * kRowsMax + row) * kFeat + li] = accs[f][r];
+            }
+        }
+}
+
+template <int ET, int XR, int UMAX, int NWR, int NXR>
+__global__ __launch_bounds__(kWaves * 64, 1) void batched_decode_kernel(
+    const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
+    const uint32_t* __restrict__ packed, const float* __restrict__ alpha,
+    const int32_t* __restrict__ tenant_ids, int T, void* __restrict__ y, int y_dtype) {
+    using L = BatchedLayout<XR, UMAX, NWR, NXR>;
+    __shared__ __attribute__((aligned(16))) char lds[L::kTotal];
+    Routing& rt = *reinterpret_cast<Routing*>(lds + L::kRouteOff);
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n0 = blockIdx.x * kFeat;
+    constexpr uint32_t kKeyInvalid = 0x80000000u, kKeyPad = 0x80000001u;
+
+    for (int i = threadIdx.x; i < kRowsMax * 16; i += kWaves * 64) (&rt.frag_row[0][0])[i] = -1;
+    // ---- routing (wave 0): stable sort of the rows by tenant ----
+    if (wv == 0) {
+        uint32_t key = kKeyPad;
+        if (lane < M) {
+            const int t = tenant_ids[lane];
+            key = (t >= 0 && t < T) ? (uint32_t)t : kKeyInvalid;
+        }
+        int rank = 0;
+        for (int j = 0; j < kRowsMax; ++j) {
+            const uint32_t kj = __builtin_amdgcn_readlane(key, j);
+            rank += (kj < key || (kj == key && j < lane)) ? 1 : 0;
+        }
+        rt.sorted_row[rank] = lane < M ? lane : 0;
+        rt.key_sorted[rank] = key;
+        rt.tenant_of_row[lane] = key < kKeyInvalid ? (int)key : -1;
+        rt.frag_of_row[lane] = -1;
+    }
+    __syncthreads();
+    // ---- fragments (runs of up to 16 rows of one tenant) and sign slots ----
+    if (wv == 0) {
+        const int p = lane;
+        const uint32_t kp = rt.key_sorted[p];
+        const uint32_t kprev = p > 0 ? rt.key_sorted[p - 1] : 0xFFFFFFFFu;
+        const bool valid = kp < kKeyInvalid;
+        const unsigned long long upto = p == 63 ? ~0ull : ((2ull << p) - 1ull);
+        const unsigned long long tstart = __ballot(valid && kp != kprev);
+        const int first = 63 - __builtin_clzll((tstart & upto) | 1ull);
+        const int rank = p - first;
+        const int slot = __popcll(tstart & upto) - 1;
+        const unsigned long long fstart = __ballot(valid && (rank & 15) == 0);
+        const int fidx = __popcll(fstart & upto) - 1;
+        if (valid) {
+            rt.frag_row[fidx][rank & 15] = rt.sorted_row[p];
+            rt.frag_of_row[rt.sorted_row[p]] = fidx;
+            if ((rank & 15) == 0) rt.frag_slot[fidx] = slot;
+            if (rank == 0 && slot < 16) rt.slot_tenant[slot] = (int)kp;
+        }
+        if (lane == 0) {
+            rt.nfrag = __popcll(fstart);
+            rt.nslot = __popcll(tstart);
+        }
+    }
+    __syncthreads();
+    const int F = rt.nfrag;
+
+    // ---- main loop, specialised for the fragment count; passes of FMAX fragments ----
+    // fragments per pass: all of them up to 16 (12 for 64 rows x 16 tenants, to fit registers)
+    constexpr int FMAX = (XR == 64 && UMAX == 16) ? 12 : ((XR / 16 + UMAX) < 16 ? (XR / 16 + UMAX) : 16);
+    const float* red_b = reinterpret_cast<const float*>(lds);
+    const float* red_s = red_b + kWaves * kRowsMax * kFeat;
+    for (int f0 = 0; f0 < F; f0 += FMAX) {
+        const int fc = min(FMAX, F - f0);
+        static_for<FMAX>([&](auto ic) {
+            constexpr int FC = decltype(ic)::value + 1;
+            if (fc == FC) batched_loop<ET, XR, UMAX, NWR, NXR, FC>(lds, rt, x, M, K, w, N, packed, n0, lane, wv, f0);
+        });
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < M * kFeat; idx += kWaves * 64) {
+            const int m = idx >> 4, ff = idx & 15;
+            const int nn = n0 + ff;
+            const int fr = rt.frag_of_row[m];
+            if (nn >= N || fr < f0 || fr >= f0 + fc) continue;
+            float bsum = 0.f, ssum = 0.f;
+#pragma unroll
+            for (int v = 0; v < kWaves; ++v) {
+                bsum += red_b[(v * kRowsMax + m) * kFeat + ff];
+                ssum += red_s[(v * kRowsMax + m) * kFeat + ff];
+            }
+            store_y<ET>(y, (size_t)m * N + nn, __builtin_fmaf(alpha[rt.tenant_of_row[m]], ssum, bsum), y_dtype);
+        }
+        __syncthreads();        // the next pass reuses the rings
+    }
+    // rows whose tenant id is out of range
+    for (int idx = threadIdx.x; idx < M * kFeat; idx += kWaves * 64) {
+        const int m = idx >> 4, nn = n0 + (idx & 15);
+        if (nn < N && rt.tenant_of_row[m] < 0) store_y<ET>(y, (size_t)m * N + nn, __builtin_nanf(""), y_dtype);
+    }
+}
+
+template <int ET, int XR, int UMAX, int NWR, int NXR>
+hipError_t launch_cfg(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                      const uint32_t* packed, const float* alpha, const int32_t* tenant_ids, int T,
+                      void* y, int y_dtype, hipStream_t stream) {
+    const int grid = (N + kFeat - 1) / kFeat;
+    batched_decode_kernel<ET, XR, UMAX, NWR, NXR><<<grid, kWaves * 64, 0, stream>>>(
+        x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype);
+    return hipGetLastError();
+}
+
+template <int ET>
+hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                     const uint32_t* packed, const float* alpha, const int32_t* tenant_ids, int T,
+                     void* y, int y_dtype, hipStream_t stream) {
+    const int u = min(T, M);
+    const int xr = (M + 15) / 16 * 16;
+    // LDS: signs 2 x UMAX x 2 KB, x NXR x XR x 512 B, W NWR x 8 KB, routing tables
+    // about 5 KB, at most 160 KB.  Measured at 64 rows x 4096 x 4096 and 32 rows x
+    // 11008 x 4096, ring depths between 2 and 7 tiles move the time by under 5%.
+    if (u <= 8) {
+        if (xr <= 16) return launch_cfg<ET, 16, 8, 8, 4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        if (xr <= 32) return launch_cfg<ET, 32, 8, 6, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        return launch_cfg<ET, 64, 8, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    }
+    if (xr <= 16) return launch_cfg<ET, 16, 16, 6, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    if (xr <= 32) return launch_cfg<ET, 32, 16, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    return launch_cfg<ET, 64, 16, 3, 2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+}
+
+}  // namespace
+
+bool batched_supported(int M, int N, int K, int T) {
+    return M >= 1 && M <= kRowsMax && min(T, M) <= 16 && K >= kTileK && K % kTileK == 0;
+}
+
+hipError_t launch_batched(const uint16_t* x, int M, int K, const uint16_t* w, int N,
+                          const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,
+                          int T, void* y, int y_dtype, int et, hipStream_t stream) {
+    if (et == kF16)
+        return launch_et<kF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    return launch_et<kBF16>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+}
+
+}  // namespace bitdelta

@@ -58,9 +58,17 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
 // The byte is first duplicated 15 bits higher, so one left shift brings bit 2j
 // to position 15 and bit 2j+1 to position 31 at once; one 3-input bit op then
 // flips the sign bits of the packed (-1, -1) constant: two values per two ops.
+// Hides a value from the optimiser so that the shift-and-mask sequences built
+// on it are emitted as written (left alone, it folds byte | byte << 15 and the
+// following shifts into quarter-rate integer multiplies).
+__device__ __forceinline__ uint32_t opaque_u32(uint32_t v) {
+    asm("" : "+v"(v));
+    return v;
+}
+
 template <int ET>
 __device__ __forceinline__ u32x4 decode_signs8(uint32_t byte) {
-    const uint32_t s = byte | (byte << 15);
+    const uint32_t s = opaque_u32(byte | (byte << 15));
     u32x4 r;
     r[0] = kMinusOnePair<ET> ^ ((s << 15) & kSignBits);
     r[1] = kMinusOnePair<ET> ^ ((s << 13) & kSignBits);
@@ -98,7 +106,7 @@ __device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
 }
 
 __device__ __forceinline__ u32x4 fuse_weights8_f16(u32x4 w, uint32_t byte, uint32_t neg_alpha_pair) {
-    const uint32_t s = byte | (byte << 15);
+    const uint32_t s = opaque_u32(byte | (byte << 15));
     u32x4 r;
 #pragma unroll
     for (int j = 0; j < 4; ++j) r[j] = add_f16x2(w[j], neg_alpha_pair ^ ((s << (15 - 2 * j)) & kSignBits));

@@ -1,0 +1,131 @@
+"""Parity of the batched decode kernel (rows gathered per tenant, one sign
+decode per tenant and k-block) with the fp64 oracle.
+
+The kernel serves batched requests with at most 64 rows, at most 16 distinct
+tenants (min(T, M) <= 16) and K a multiple of 256.  Cases cover each of its
+row / tenant-slot configurations (up to 16, 32 and 64 rows; up to 8 and 16
+tenants), a K that ends inside a 1024-k sign super-tile, more row fragments
+than one pass holds, out-of-range ids, the exact decode-isolating forms and
+run-to-run determinism.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from gpu_util import dev_half, dev_f32, dev_i32, dev_words, host_out, log, run_matmul, torch
+from tolerance import check
+
+pytestmark = pytest.mark.gpu
+
+SKINNY = 1
+
+
+def oracle_y(p, tid=None):
+    tid = p.tenant_ids if tid is None else tid
+    return oracle.matmul(p.x, p.w, p.packed, p.alpha, tid)
+
+
+CASES = [  # M, N, K, T
+    (1, 80, 256, 3), (5, 48, 256, 2), (16, 40, 512, 16), (13, 70, 768, 11),
+    (24, 50, 1024, 8), (32, 100, 768, 16), (17, 33, 1280, 12), (33, 17, 2304, 9),
+    (48, 20, 256, 5), (64, 64, 512, 8), (64, 40, 512, 16), (64, 96, 4096, 8),
+    (8, 40, 11008, 4), (64, 30, 11008, 8),
+]
+
+
+@pytest.mark.parametrize("M,N,K,T", CASES)
+@pytest.mark.parametrize("yd", ["f32", "bf16"])
+def test_batched_ragged(M, N, K, T, yd):
+    p = wl.make_problem(M, N, K, T, seed=M * 5 + N + K + T, multi_tenant=True, y_dtype=yd)
+    log(f"batched M={M} N={N} K={K} T={T} {yd} tenants present {len(np.unique(p.tenant_ids))}")
+    y = host_out(run_matmul(p, path=SKINNY))
+    relf, _ = check(y, oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    if yd == "f32":
+        assert relf < 1e-5, relf
+
+
+@pytest.mark.parametrize("M,T,counts", [
+    (64, 16, [1] * 15 + [49]),          # 15 + 4 = 19 fragments: two passes of 12
+    (64, 16, [4] * 16),                 # 16 fragments of 4 rows
+    (32, 16, [17, 15] + [0] * 14),      # one tenant split over two fragments
+    (64, 8, [64] + [0] * 7),            # one tenant, four fragments
+])
+def test_batched_fragment_layouts(M, T, counts):
+    p = wl.make_problem(M, 60, 1024, T, seed=M + T + len(counts), multi_tenant=True, y_dtype="f32")
+    ids = np.repeat(np.arange(T), counts).astype(np.int32)
+    p.tenant_ids = np.random.default_rng(sum(counts[:3])).permutation(ids)
+    log(f"batched fragments M={M} T={T} counts={counts}")
+    y = host_out(run_matmul(p, path=SKINNY))
+    relf, _ = check(y, oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    assert relf < 1e-5, relf
+
+
+def test_batched_invalid_ids_are_nan_rows():
+    M, N, K, T = 40, 50, 512, 6
+    p = wl.make_problem(M, N, K, T, seed=31, multi_tenant=True, y_dtype="f32")
+    tid = p.tenant_ids.copy()
+    tid[[0, 7, 39]] = [-1, T, 1 << 30]
+    p.tenant_ids = tid
+    log("batched invalid ids")
+    y = host_out(run_matmul(p, path=SKINNY))
+    bad = (tid < 0) | (tid >= T)
+    assert np.all(np.isnan(y[bad]))
+    ref = oracle_y(p, np.where(bad, 0, tid))
+    relf, _ = check(y[~bad], ref[~bad], p.x[~bad], p.w, p.alpha, tid[~bad])
+    assert relf < 1e-5, relf
+
+
+@pytest.mark.parametrize("a", [1.0, 2.0 ** -10])
+def test_batched_ones_zero_weight_exact(a):
+    # x = 1, W = 0: y[m, n] = alpha_t * (2 popcount(S_t[n]) - K) exactly, per tenant
+    rng = np.random.default_rng(8)
+    M, N, K, T = 20, 48, 2048, 5
+    packed = wl.uniform_words(rng, (T, N, K // 32))
+    alpha = (a * (1 + np.arange(T))).astype(np.float32)
+    tid = (np.arange(M) % T).astype(np.int32)
+    p = wl.Problem("ones", np.full((M, K), 0x3F80, np.uint16), np.zeros((N, K), np.uint16),
+                   alpha, packed=packed, tenant_ids=tid, y_dtype="f32")
+    log(f"batched ones/zero-weight exact alpha={a}")
+    y = host_out(run_matmul(p, path=SKINNY))
+    pc = np.array([[sum(int(v).bit_count() for v in packed[t, n]) for n in range(N)] for t in range(T)])
+    ref = alpha[tid][:, None].astype(np.float64) * (2 * pc[tid] - K)
+    assert np.array_equal(y, ref)
+
+
+def test_batched_one_hot_rows_every_bit_position():
+    # x = e_k (row k), tenants alternating: y[k, n] = W[n, k] + alpha_t * s_t[n, k]
+    K, N, T = 256, 40, 3
+    base = wl.make_problem(1, N, K, T, seed=9, multi_tenant=True)
+    rows = np.arange(64)
+    for k0 in (0, 64, 128, 192):
+        x = np.zeros((64, K), np.uint16)
+        x[rows, k0 + rows] = 0x3F80
+        tid = (rows % T).astype(np.int32)
+        p = wl.Problem("onehot", x, base.w, base.alpha, packed=base.packed, tenant_ids=tid, y_dtype="f32")
+        log(f"batched one-hot rows k0={k0}")
+        y = host_out(run_matmul(p, path=SKINNY))
+        ref = oracle.matmul(x, p.w, p.packed, p.alpha, tid)
+        np.testing.assert_allclose(y, ref, rtol=2.0 ** -23, atol=0)
+
+
+def test_batched_deterministic():
+    p = wl.make_problem(64, 300, 4096, 8, seed=33, multi_tenant=True, y_dtype="bf16")
+    log("batched determinism")
+    y1 = run_matmul(p, path=SKINNY).view(torch().int16).cpu().numpy()
+    y2 = run_matmul(p, path=SKINNY).view(torch().int16).cpu().numpy()
+    assert np.array_equal(y1, y2)
+
+
+def test_batched_f16():
+    import paper_2609_36800_amd as bd
+    t = torch()
+    p = wl.make_problem(48, 90, 1536, 7, seed=34, multi_tenant=True, y_dtype="f32", dtype="f16")
+    log("batched f16")
+    y = bd.matmul(dev_half(p.x, "f16"), dev_half(p.w, "f16"), dev_words(p.packed), dev_f32(p.alpha),
+                  tenant_ids=dev_i32(p.tenant_ids), out_dtype=t.float32, path=SKINNY)
+    t.cuda.synchronize()
+    y = host_out(y)
+    ref = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids, dtype="f16")
+    relf, _ = check(y, ref, p.x, p.w, p.alpha, p.tenant_ids, dtype="f16")
+    assert relf < 1e-5, relf
