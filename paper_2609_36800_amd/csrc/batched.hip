@@ -55,16 +55,6 @@ constexpr int kRowBytes = kTileK * 2;          // 512 B of one row per tile
 constexpr int kSuperTiles = 4;                 // tiles per sign super-tile
 constexpr int kSignRowBytes = kSuperTiles * kTileK / 8;   // 128 B of sign bits per row
 
-// Calls f(integral_constant<int, i>) for i = 0 .. N-1.
-template <typename Fn, int... Is>
-__device__ __forceinline__ void static_for_impl(Fn&& f, std::integer_sequence<int, Is...>) {
-    (f(std::integral_constant<int, Is>{}), ...);
-}
-template <int N, typename Fn>
-__device__ __forceinline__ void static_for(Fn&& f) {
-    static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
 __device__ __forceinline__ int swz16(int row, int chunk) { return chunk ^ (row & 15); }
 __device__ __forceinline__ int swz8(int row, int chunk) { return chunk ^ (row & 7); }
 

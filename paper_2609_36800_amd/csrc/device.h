@@ -16,9 +16,22 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <utility>
+
 #include "internal.h"
 
 namespace bitdelta {
+
+// Calls f(integral_constant<int, i>) for i = 0 .. N-1 (indices usable as
+// compile-time register-array subscripts).
+template <typename Fn, int... Is>
+__device__ __forceinline__ void static_for_impl(Fn&& f, std::integer_sequence<int, Is...>) {
+    (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, typename Fn>
+__device__ __forceinline__ void static_for(Fn&& f) {
+    static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // Kernels templated on ET (the 16-bit element type of x and W: kBF16 or
 // kF16) use the matching matrix instruction, +-1 constant and rounding.
