@@ -1,4 +1,4 @@
-// Batched (multi-tenant) binary-delta matmul for at most 64 token rows with at
+// Batched (multi-tenant) binary-delta matmul for 33 to 64 token rows with at
 // most 16 distinct tenants per call, K a multiple of 256:
 //
 //   y[m][n] = sum_k x[m][k] W[n][k] + alpha[t(m)] * sum_k x[m][k] s_t(m)[n][k]
@@ -347,25 +347,20 @@ template <int ET>
 hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                      const uint32_t* packed, const float* alpha, const int32_t* tenant_ids, int T,
                      void* y, int y_dtype, hipStream_t stream) {
-    const int u = min(T, M);
-    const int xr = (M + 15) / 16 * 16;
-    // LDS: signs 2 x UMAX x 2 KB, x NXR x XR x 512 B, W NWR x 8 KB, routing tables
-    // about 5 KB, at most 160 KB.  Measured at 64 rows x 4096 x 4096 and 32 rows x
-    // 11008 x 4096, ring depths between 2 and 7 tiles move the time by under 5%.
-    if (u <= 8) {
-        if (xr <= 16) return launch_cfg<ET, 16, 8, 8, 4>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-        if (xr <= 32) return launch_cfg<ET, 32, 8, 6, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    // LDS: signs 2 x UMAX x 2 KB, x NXR x 64 x 512 B, W NWR x 8 KB, routing tables
+    // about 5 KB, at most 160 KB.  Measured at 64 rows x 4096 x 4096, ring depths
+    // between 2 and 7 tiles move the time by under 5%.
+    if (min(T, M) <= 8)
         return launch_cfg<ET, 64, 8, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-    }
-    if (xr <= 16) return launch_cfg<ET, 16, 16, 6, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
-    if (xr <= 32) return launch_cfg<ET, 32, 16, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
     return launch_cfg<ET, 64, 16, 3, 2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
 }
 
 }  // namespace
 
 bool batched_supported(int M, int N, int K, int T) {
-    return M >= 1 && M <= kRowsMax && min(T, M) <= 16 && K >= kTileK && K % kTileK == 0;
+    // 33 to 64 rows: below that the tenant-slot kernel (multi.hip) measures as fast
+    // or faster, since a fragment then carries only a row or two
+    return M > 32 && M <= kRowsMax && min(T, M) <= 16 && K >= kTileK && K % kTileK == 0;
 }
 
 hipError_t launch_batched(const uint16_t* x, int M, int K, const uint16_t* w, int N,

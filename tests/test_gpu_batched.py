@@ -1,12 +1,12 @@
-"""Parity of the batched decode kernel (rows gathered per tenant, one sign
-decode per tenant and k-block) with the fp64 oracle.
+"""Parity of the batched decode-shaped kernels with the fp64 oracle.
 
-The kernel serves batched requests with at most 64 rows, at most 16 distinct
-tenants (min(T, M) <= 16) and K a multiple of 256.  Cases cover each of its
-row / tenant-slot configurations (up to 16, 32 and 64 rows; up to 8 and 16
-tenants), a K that ends inside a 1024-k sign super-tile, more row fragments
-than one pass holds, out-of-range ids, the exact decode-isolating forms and
-run-to-run determinism.
+Batched requests with 33 to 64 rows, at most 16 distinct tenants and K a
+multiple of 256 take the kernel that gathers each tenant's rows into 16-row
+fragments (one sign decode per tenant and k-block); fewer rows take the
+tenant-slot kernel.  Cases cover both tenant-slot configurations of the
+gathered kernel (up to 8 and up to 16 tenants), a K that ends inside a 1024-k
+sign super-tile, more row fragments than one pass holds, out-of-range ids, the
+exact decode-isolating forms, fp16 and run-to-run determinism.
 """
 import numpy as np
 import pytest
@@ -27,10 +27,10 @@ def oracle_y(p, tid=None):
 
 
 CASES = [  # M, N, K, T
-    (1, 80, 256, 3), (5, 48, 256, 2), (16, 40, 512, 16), (13, 70, 768, 11),
-    (24, 50, 1024, 8), (32, 100, 768, 16), (17, 33, 1280, 12), (33, 17, 2304, 9),
-    (48, 20, 256, 5), (64, 64, 512, 8), (64, 40, 512, 16), (64, 96, 4096, 8),
-    (8, 40, 11008, 4), (64, 30, 11008, 8),
+    (1, 80, 256, 3), (16, 40, 512, 16), (32, 100, 768, 16),
+    (33, 17, 2304, 9), (40, 70, 768, 11), (48, 20, 256, 5), (56, 50, 1024, 16),
+    (64, 64, 512, 8), (64, 40, 512, 16), (64, 96, 4096, 8), (64, 30, 11008, 8),
+    (36, 40, 11008, 4), (64, 33, 1280, 12), (64, 20, 512, 64),
 ]
 
 
@@ -48,7 +48,7 @@ def test_batched_ragged(M, N, K, T, yd):
 @pytest.mark.parametrize("M,T,counts", [
     (64, 16, [1] * 15 + [49]),          # 15 + 4 = 19 fragments: two passes of 12
     (64, 16, [4] * 16),                 # 16 fragments of 4 rows
-    (32, 16, [17, 15] + [0] * 14),      # one tenant split over two fragments
+    (48, 16, [17, 31] + [0] * 14),      # tenants split over two fragments
     (64, 8, [64] + [0] * 7),            # one tenant, four fragments
 ])
 def test_batched_fragment_layouts(M, T, counts):
@@ -80,7 +80,7 @@ def test_batched_invalid_ids_are_nan_rows():
 def test_batched_ones_zero_weight_exact(a):
     # x = 1, W = 0: y[m, n] = alpha_t * (2 popcount(S_t[n]) - K) exactly, per tenant
     rng = np.random.default_rng(8)
-    M, N, K, T = 20, 48, 2048, 5
+    M, N, K, T = 40, 48, 2048, 5
     packed = wl.uniform_words(rng, (T, N, K // 32))
     alpha = (a * (1 + np.arange(T))).astype(np.float32)
     tid = (np.arange(M) % T).astype(np.int32)
