@@ -1,5 +1,6 @@
-// Batched (multi-tenant) binary-delta matmul for 33 to 64 token rows with at
-// most 16 distinct tenants per call, K a multiple of 256:
+// Batched (multi-tenant) binary-delta matmul for up to 64 token rows with at
+// most 16 distinct tenants per call, K a multiple of 256 (the dispatcher sends
+// it 33 to 64 rows, and 17 to 32 when the grid is one workgroup per CU):
 //
 //   y[m][n] = sum_k x[m][k] W[n][k] + alpha[t(m)] * sum_k x[m][k] s_t(m)[n][k]
 //
@@ -18,7 +19,10 @@
 // block a fragment costs one x fragment read, one sign decode and two MFMAs
 // (x*W^T and x*S_t^T on the gathered rows).  F is known only on the device:
 // every workgroup computes the routing (wave 0, ballots) and enters the loop
-// specialised for its F.
+// specialised for its F.  Sign slot u holds tenant u when there are at most
+// as many tenants as slots, so the first tiles' copies go out before the
+// routing is known; with more tenants the slots are compacted to the tenants
+// present and the copies wait for the routing.
 //
 // Memory path.  A 512-thread workgroup owns 16 output features; K runs in
 // 256-k tiles and wave w computes k-block w of every tile.  All operands reach
@@ -54,6 +58,7 @@ constexpr int kTileK = 256;                    // k per tile (one 32-k block per
 constexpr int kRowBytes = kTileK * 2;          // 512 B of one row per tile
 constexpr int kSuperTiles = 4;                 // tiles per sign super-tile
 constexpr int kSignRowBytes = kSuperTiles * kTileK / 8;   // 128 B of sign bits per row
+constexpr int kResidentWorkgroups = 256;       // one per CU on MI355X (160 KB LDS each)
 
 __device__ __forceinline__ int swz16(int row, int chunk) { return chunk ^ (row & 15); }
 __device__ __forceinline__ int swz8(int row, int chunk) { return chunk ^ (row & 7); }
@@ -90,65 +95,100 @@ struct BatchedLayout {
     static_assert(NXR >= 2 && NWR >= NXR, "ring depths");
 };
 
-template <int ET, int XR, int UMAX, int NWR, int NXR, int F>
-__device__ __forceinline__ void batched_loop(char* lds, const Routing& rt, const uint16_t* __restrict__ x,
-                                             int M, int K, const uint16_t* __restrict__ w, int N,
-                                             const uint32_t* __restrict__ packed, int n0, int lane, int wv,
-                                             int f0) {
+// The global->LDS copies of one wave's share of the rings: W rows, x rows and
+// sign rows of copy-wave index cw (normally the wave's own index; another wave
+// can issue a share on its behalf).  All sources are clamped in range; surplus
+// rows feed unstored outputs.  tenant_of_slot(u) gives the tenant whose sign
+// rows fill slot u.
+template <int XR, int UMAX, int NWR, int NXR>
+struct Copier {
     using L = BatchedLayout<XR, UMAX, NWR, NXR>;
-    const int li = lane & 15, g = lane >> 4;
-    const int KW = K >> 5, KT = K / kTileK;
-    const int NS = (KT + kSuperTiles - 1) / kSuperTiles;
-
-    // ---- copy sources (all clamped in range; surplus rows feed unstored outputs) ----
-    // W: wave w copies rows 2w, 2w+1 (lane >> 5), 16-byte chunk (lane & 31) swizzled
-    const int wrow = 2 * wv + (lane >> 5);
-    const uint16_t* wsrc = w + (size_t)min(n0 + wrow, N - 1) * K + 8 * swz16(wrow, lane & 31);
-    // x: wave w copies rows 2(w*XOPS + i) + (lane >> 5)
+    static constexpr int DX = NXR - 1, DW = NWR - 1;
+    char* lds;
+    int cw, KT, KW, NS, schunk;
+    const uint16_t* wsrc;
     const uint16_t* xsrc[L::kXOps];
-#pragma unroll
-    for (int i = 0; i < L::kXOps; ++i) {
-        const int r = 2 * (wv * L::kXOps + i) + (lane >> 5);
-        xsrc[i] = x + (size_t)min(r, M - 1) * K + 8 * swz16(r, lane & 31);
-    }
-    // signs: the UMAX*16 (slot, feature) rows of a super-tile, 8 per copy with 8
-    // lanes per row; half h holds rows [h*UMAX*8, (h+1)*UMAX*8), copy j of wave w
-    // its rows 8*(w*kSOps + j) .. +7
     int srow[2][L::kSOps];
     const uint32_t* ssrc[2][L::kSOps];
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int j = 0; j < L::kSOps; ++j) {
-            srow[h][j] = h * UMAX * 8 + 8 * (wv * L::kSOps + j) + (lane >> 3);
-            const int u = srow[h][j] >> 4, f = srow[h][j] & 15;
-            const int t = rt.slot_tenant[min(u, rt.nslot - 1)];
-            ssrc[h][j] = packed + ((size_t)t * N + min(n0 + f, N - 1)) * KW;
-        }
-    const int schunk = lane & 7;
 
-    auto issue_x = [&](int tt) {
+    template <class SlotFn>
+    __device__ __forceinline__ Copier(char* lds_, int cw_, int lane, const uint16_t* __restrict__ x, int M, int K,
+                                      const uint16_t* __restrict__ w, int N, const uint32_t* __restrict__ packed,
+                                      int n0, SlotFn tenant_of_slot)
+        : lds(lds_), cw(cw_) {
+        KT = K / kTileK;
+        KW = K >> 5;
+        NS = (KT + kSuperTiles - 1) / kSuperTiles;
+        // W: copy-wave c copies rows 2c, 2c+1 (lane >> 5), 16-byte chunk (lane & 31) swizzled
+        const int wrow = 2 * cw + (lane >> 5);
+        wsrc = w + (size_t)min(n0 + wrow, N - 1) * K + 8 * swz16(wrow, lane & 31);
+        // x: copy-wave c copies rows 2(c*XOPS + i) + (lane >> 5)
+#pragma unroll
+        for (int i = 0; i < L::kXOps; ++i) {
+            const int r = 2 * (cw * L::kXOps + i) + (lane >> 5);
+            xsrc[i] = x + (size_t)min(r, M - 1) * K + 8 * swz16(r, lane & 31);
+        }
+        // signs: the UMAX*16 (slot, feature) rows of a super-tile, 8 per copy with 8
+        // lanes per row; half h holds rows [h*UMAX*8, (h+1)*UMAX*8), copy j of
+        // copy-wave c its rows 8*(c*kSOps + j) .. +7
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int j = 0; j < L::kSOps; ++j) {
+                srow[h][j] = h * UMAX * 8 + 8 * (cw * L::kSOps + j) + (lane >> 3);
+                const int u = srow[h][j] >> 4, f = srow[h][j] & 15;
+                ssrc[h][j] = packed + ((size_t)tenant_of_slot(u) * N + min(n0 + f, N - 1)) * KW;
+            }
+        schunk = lane & 7;
+    }
+    __device__ __forceinline__ void issue_x(int tt) const {
         const int tc = min(tt, KT - 1);
         char* buf = lds + L::kXOff + (tt % NXR) * L::kX;
 #pragma unroll
         for (int i = 0; i < L::kXOps; ++i)
-            copy16_to_lds(xsrc[i] + (size_t)tc * kTileK, buf + (wv * L::kXOps + i) * 1024);
-    };
-    auto issue_w = [&](int tt) {
+            copy16_to_lds(xsrc[i] + (size_t)tc * kTileK, buf + (cw * L::kXOps + i) * 1024);
+    }
+    __device__ __forceinline__ void issue_w(int tt) const {
         const int tc = min(tt, KT - 1);
-        copy16_to_lds(wsrc + (size_t)tc * kTileK, lds + L::kWOff + (tt % NWR) * L::kW + wv * 1024);
-    };
+        copy16_to_lds(wsrc + (size_t)tc * kTileK, lds + L::kWOff + (tt % NWR) * L::kW + cw * 1024);
+    }
     // half h of super-tile s
-    auto issue_s = [&](int s, int h) {
+    __device__ __forceinline__ void issue_s(int s, int h) const {
         const int sc = min(s, NS - 1);
 #pragma unroll
         for (int j = 0; j < L::kSOps; ++j) {
             const int c = swz8(srow[h][j], schunk);                // source chunk at this position
             const int word = min(32 * sc + 4 * c, KW - 4);
-            const int drow = h * UMAX * 8 + 8 * (wv * L::kSOps + j);     // first row of this copy
+            const int drow = h * UMAX * 8 + 8 * (cw * L::kSOps + j);     // first row of this copy
             copy16_to_lds(ssrc[h][j] + word, lds + L::kSOff + (s & 1) * L::kS + drow * kSignRowBytes);
         }
-    };
+    }
+    // prologue: super-tile 0, then x(0 .. DX-1) and W(0 .. DW-1)
+    __device__ __forceinline__ void prologue_s() const {
+        issue_s(0, 0);
+        issue_s(0, 1);
+    }
+    __device__ __forceinline__ void prologue_xw(bool do_x, bool do_w) const {
+#pragma unroll
+        for (int i = 0; i < DW; ++i) {
+            if (do_x && i < DX) issue_x(i);
+            if (do_w) issue_w(i);
+        }
+    }
+};
+
+// One pass over K for fragments f0 .. f0+F-1.  With `issued` the prologue
+// copies (super-tile 0, x(0 .. DX-1), W(0 .. DW-1)) are already in flight.
+template <int ET, int XR, int UMAX, int NWR, int NXR, int F>
+__device__ __forceinline__ void batched_loop(char* lds, const Routing& rt, const uint16_t* __restrict__ x,
+                                             int M, int K, const uint16_t* __restrict__ w, int N,
+                                             const uint32_t* __restrict__ packed, int n0, int lane, int wv,
+                                             int f0, bool issued) {
+    using L = BatchedLayout<XR, UMAX, NWR, NXR>;
+    const int li = lane & 15, g = lane >> 4;
+    const int KT = K / kTileK;
+    const Copier<XR, UMAX, NWR, NXR> cp(lds, wv, lane, x, M, K, w, N, packed, n0,
+                                        [&](int u) { return rt.slot_tenant[min(u, rt.nslot - 1)]; });
 
     // ---- fragment read offsets ----
     const int wchunk = 4 * wv + g;                                  // this lane's chunk of a tile row
@@ -174,12 +214,9 @@ __device__ __forceinline__ void batched_loop(char* lds, const Routing& rt, const
 
     // ---- prologue: super-tile 0, then the issue groups of tiles 0 .. NXR-2 / NWR-2 ----
     constexpr int DX = NXR - 1, DW = NWR - 1;
-    issue_s(0, 0);
-    issue_s(0, 1);
-#pragma unroll
-    for (int i = 0; i < DW; ++i) {
-        if (i < DX) issue_x(i);
-        issue_w(i);
+    if (!issued) {
+        cp.prologue_s();
+        cp.prologue_xw(true, true);
     }
     __builtin_amdgcn_sched_barrier(0);
 
@@ -194,9 +231,9 @@ __device__ __forceinline__ void batched_loop(char* lds, const Routing& rt, const
         else wait_vm_lgkm0<kWait>();
         raw_barrier();
         // issue group: sign half (t&3 < 2 ? t&3 : 1) of super-tile t/4+1, x(t+DX), W(t+DW)
-        issue_s((t >> 2) + 1, min(t & 3, 1));
-        issue_x(t + DX);
-        issue_w(t + DW);
+        cp.issue_s((t >> 2) + 1, min(t & 3, 1));
+        cp.issue_x(t + DX);
+        cp.issue_w(t + DW);
         __builtin_amdgcn_sched_barrier(0);
 
         const int kb = t * 8 + wv;
@@ -253,6 +290,24 @@ __global__ __launch_bounds__(kWaves * 64, 1) void batched_decode_kernel(
     const int n0 = blockIdx.x * kFeat;
     constexpr uint32_t kKeyInvalid = 0x80000000u, kKeyPad = 0x80000001u;
 
+    // ---- with at most UMAX tenants, sign slot u holds tenant u (absent tenants'
+    //      slots are copied and not read), so the first tiles' copies do not
+    //      depend on the routing and go out now, while wave 0 routes.  Wave 0's
+    //      share is issued by waves 5..7: its id load must not queue behind
+    //      copies of its own. ----
+    const bool ident = T <= UMAX;
+    if (ident && wv != 0) {
+        auto ident_slot = [&](int u) { return min(u, T - 1); };
+        const Copier<XR, UMAX, NWR, NXR> own(lds, wv, lane, x, M, K, w, N, packed, n0, ident_slot);
+        own.prologue_s();
+        own.prologue_xw(true, true);
+        if (wv >= 5) {
+            const Copier<XR, UMAX, NWR, NXR> w0(lds, 0, lane, x, M, K, w, N, packed, n0, ident_slot);
+            if (wv == 5) w0.prologue_s();
+            w0.prologue_xw(wv == 6, wv == 7);
+        }
+    }
+
     for (int i = threadIdx.x; i < kRowsMax * 16; i += kWaves * 64) (&rt.frag_row[0][0])[i] = -1;
     // ---- routing (wave 0): stable sort of the rows by tenant ----
     if (wv == 0) {
@@ -282,18 +337,19 @@ __global__ __launch_bounds__(kWaves * 64, 1) void batched_decode_kernel(
         const unsigned long long tstart = __ballot(valid && kp != kprev);
         const int first = 63 - __builtin_clzll((tstart & upto) | 1ull);
         const int rank = p - first;
-        const int slot = __popcll(tstart & upto) - 1;
+        const int slot = ident ? (int)kp : __popcll(tstart & upto) - 1;
         const unsigned long long fstart = __ballot(valid && (rank & 15) == 0);
         const int fidx = __popcll(fstart & upto) - 1;
         if (valid) {
             rt.frag_row[fidx][rank & 15] = rt.sorted_row[p];
             rt.frag_of_row[rt.sorted_row[p]] = fidx;
             if ((rank & 15) == 0) rt.frag_slot[fidx] = slot;
-            if (rank == 0 && slot < 16) rt.slot_tenant[slot] = (int)kp;
+            if (!ident && rank == 0 && slot < 16) rt.slot_tenant[slot] = (int)kp;
         }
+        if (ident && lane < T) rt.slot_tenant[lane] = lane;
         if (lane == 0) {
             rt.nfrag = __popcll(fstart);
-            rt.nslot = __popcll(tstart);
+            rt.nslot = ident ? T : __popcll(tstart);
         }
     }
     __syncthreads();
@@ -308,7 +364,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void batched_decode_kernel(
         const int fc = min(FMAX, F - f0);
         static_for<FMAX>([&](auto ic) {
             constexpr int FC = decltype(ic)::value + 1;
-            if (fc == FC) batched_loop<ET, XR, UMAX, NWR, NXR, FC>(lds, rt, x, M, K, w, N, packed, n0, lane, wv, f0);
+            if (fc == FC)
+                batched_loop<ET, XR, UMAX, NWR, NXR, FC>(lds, rt, x, M, K, w, N, packed, n0, lane, wv, f0,
+                                                         ident && f0 == 0);
         });
         __syncthreads();
         for (int idx = threadIdx.x; idx < M * kFeat; idx += kWaves * 64) {
@@ -350,6 +408,11 @@ hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
     // LDS: signs 2 x UMAX x 2 KB, x NXR x 64 x 512 B, W NWR x 8 KB, routing tables
     // about 5 KB, at most 160 KB.  Measured at 64 rows x 4096 x 4096, ring depths
     // between 2 and 7 tiles move the time by under 5%.
+    if (M <= 32) {
+        if (min(T, M) <= 8)
+            return launch_cfg<ET, 32, 8, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+        return launch_cfg<ET, 32, 16, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
+    }
     if (min(T, M) <= 8)
         return launch_cfg<ET, 64, 8, 3, 3>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
     return launch_cfg<ET, 64, 16, 3, 2>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream);
@@ -358,9 +421,13 @@ hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
 }  // namespace
 
 bool batched_supported(int M, int N, int K, int T) {
-    // 33 to 64 rows: below that the tenant-slot kernel (multi.hip) measures as fast
-    // or faster, since a fragment then carries only a row or two
-    return M > 32 && M <= kRowsMax && min(T, M) <= 16 && K >= kTileK && K % kTileK == 0;
+    // 33 to 64 rows always.  17 to 32 rows when every workgroup is resident at
+    // once (one per CU); with more workgroups the tenant-slot kernel (multi.hip,
+    // two workgroups per CU) packs the grid as well or better.  At 16 rows and
+    // below a fragment carries too few rows to gain.
+    const bool one_round = (N + kFeat - 1) / kFeat <= kResidentWorkgroups;
+    const bool rows = M > 32 || (M > 16 && one_round);
+    return rows && M <= kRowsMax && min(T, M) <= 16 && K >= kTileK && K % kTileK == 0;
 }
 
 hipError_t launch_batched(const uint16_t* x, int M, int K, const uint16_t* w, int N,

@@ -1,12 +1,15 @@
 """Parity of the batched decode-shaped kernels with the fp64 oracle.
 
-Batched requests with 33 to 64 rows, at most 16 distinct tenants and K a
-multiple of 256 take the kernel that gathers each tenant's rows into 16-row
-fragments (one sign decode per tenant and k-block); fewer rows take the
-tenant-slot kernel.  Cases cover both tenant-slot configurations of the
-gathered kernel (up to 8 and up to 16 tenants), a K that ends inside a 1024-k
-sign super-tile, more row fragments than one pass holds, out-of-range ids, the
-exact decode-isolating forms, fp16 and run-to-run determinism.
+Batched requests with 33 to 64 rows (and 17 to 32 rows when the grid is one
+workgroup per CU, at most 4096 features), at most 16 distinct
+tenants and K a multiple of 256 take the kernel that gathers each tenant's rows
+into 16-row fragments (one sign decode per tenant and k-block); other requests
+take the tenant-slot kernel.  Cases cover the 32-row and 64-row forms and both
+tenant-slot configurations of each (up to 8 and up to 16 tenants), tenant ids
+used directly as sign slots (at most that many tenants) and compacted (more),
+a K that ends inside a 1024-k sign super-tile, more row fragments than one pass
+holds, out-of-range ids, the exact decode-isolating forms, fp16 and run-to-run
+determinism.
 """
 import numpy as np
 import pytest
@@ -31,6 +34,8 @@ CASES = [  # M, N, K, T
     (33, 17, 2304, 9), (40, 70, 768, 11), (48, 20, 256, 5), (56, 50, 1024, 16),
     (64, 64, 512, 8), (64, 40, 512, 16), (64, 96, 4096, 8), (64, 30, 11008, 8),
     (36, 40, 11008, 4), (64, 33, 1280, 12), (64, 20, 512, 64),
+    (17, 60, 1024, 12), (24, 50, 2304, 5), (32, 70, 4096, 8), (32, 40, 512, 40),
+    (20, 4096, 512, 10), (20, 4112, 512, 10),
 ]
 
 
@@ -50,6 +55,9 @@ def test_batched_ragged(M, N, K, T, yd):
     (64, 16, [4] * 16),                 # 16 fragments of 4 rows
     (48, 16, [17, 31] + [0] * 14),      # tenants split over two fragments
     (64, 8, [64] + [0] * 7),            # one tenant, four fragments
+    (32, 16, [1] * 15 + [17]),          # 15 + 2 = 17 fragments: two passes of 16
+    (32, 16, [2] * 16),                 # 16 fragments of 2 rows
+    (32, 8, [32] + [0] * 7),            # one tenant, two fragments
 ])
 def test_batched_fragment_layouts(M, T, counts):
     p = wl.make_problem(M, 60, 1024, T, seed=M + T + len(counts), multi_tenant=True, y_dtype="f32")
