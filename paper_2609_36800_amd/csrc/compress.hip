@@ -98,7 +98,7 @@ __global__ __launch_bounds__(kWaves * 64) void compress_kernel(
 }
 
 constexpr int kMeanThreads = 1024;
-constexpr int kMeanUnroll = 8;
+constexpr int kMeanUnroll = 16;         // rows <= 16384 in a single round of loads
 
 __global__ __launch_bounds__(kMeanThreads) void mean_kernel(const float* __restrict__ row_abs,
                                                             int rows, double count,
