@@ -256,6 +256,53 @@ def bench_compress(dev, lib, steps, warmup):
             "TBps": per * steps / secs / 1e12}
 
 
+def context_ceilings(dev, warmup):
+    """Reference points measured in the same run with library kernels (not this
+    library's): torch's elementwise negation kernel (one buffer read, another
+    written), as a bandwidth ceiling for a large transfer and for one transfer of
+    the decode launch's size (36 MB read + 36 MB written, buffers rotating over
+    more than twice the Infinity Cache), and torch.matmul's
+    plain bf16 GEMM at 4096^3 (no decode), the matrix-core reference for the fused
+    prefill.  Context only: none of them is a figure of this library."""
+    import torch
+
+    def time_calls(calls, reps):
+        replay, graphed, graph = capture(calls, calls[:max(1, warmup)])
+        secs = timed(replay, reps) / (reps * len(calls))
+        del graph
+        return secs, graphed
+
+    out = {}
+    big = 256 << 20                                   # bf16 elements: 512 MiB
+    a = torch.empty(big, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    secs, graphed = time_calls([lambda: torch.neg(a, out=b)] * 8, 2)
+    out["elementwise_copy_512MiB"] = {"us": secs * 1e6, "GBps": 2 * a.numel() * 2 / secs / 1e9,
+                          "bytes": 2 * a.numel() * 2, "graphed": graphed}
+    del a, b
+    n36 = 4096 * 4096 + 4096 * 128 * 2              # the decode launch's W + signs, in bf16 elements
+    sets = [(torch.empty(n36, dtype=torch.bfloat16, device=dev).fill_(1.0),
+             torch.empty(n36, dtype=torch.bfloat16, device=dev)) for _ in range(16)]
+    calls = [(lambda s=s: torch.neg(s[0], out=s[1])) for s in sets] * 4
+    secs, graphed = time_calls(calls, 1)
+    out["elementwise_copy_36MB"] = {"us": secs * 1e6, "GBps": 2 * n36 * 2 / secs / 1e9, "bytes": 2 * n36 * 2,
+                        "graphed": graphed, "buffer_sets": len(sets)}
+    del sets, calls
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    x = torch.randn((4096, 4096), generator=g, device=dev).to(torch.bfloat16)
+    wt = (torch.randn((4096, 4096), generator=g, device=dev) * 0.02).to(torch.bfloat16).t().contiguous()
+    y = torch.empty((4096, 4096), dtype=torch.bfloat16, device=dev)
+    secs, graphed = time_calls([lambda: torch.matmul(x, wt, out=y)] * 10, 2)
+    fl = 2.0 * 4096 ** 3
+    out["torch_matmul_bf16_4096"] = {"us": secs * 1e6, "TFLOPs": fl / secs / 1e12,
+                                     "frac_of_bf16_peak": fl / secs / 1e12 / BF16_PEAK_TFLOPS,
+                                     "graphed": graphed}
+    del x, wt, y
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(budget_s: float):
     """fp64 oracle timed on the headline workload (the M = 1 and M = 16 pair
     against one 4096x4096 matrix), repeated until about budget_s seconds."""
@@ -496,6 +543,9 @@ def main():
         workloads.append(pf16)
         workloads.append(llama_sweep(dev, launcher, args.warmup))
         workloads.append(bench_compress(dev, launcher.lib, 50, args.warmup))
+        context = context_ceilings(dev, args.warmup)
+    else:
+        context = None
 
     cpu = None if args.no_cpu else cpu_baseline(args.cpu_budget)
 
@@ -509,6 +559,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "workloads": workloads,
+        "context": context,
     }
     print(json.dumps(out), flush=True)
 
