@@ -44,7 +44,9 @@ typedef enum {
     BITDELTA_ERR_DTYPE = -4,       /* dtype code not accepted by this argument   */
     BITDELTA_ERR_UNSUPPORTED = -5, /* valid request this path cannot serve       */
     BITDELTA_ERR_HIP = -6,         /* the HIP runtime reported a launch failure  */
-    BITDELTA_ERR_ALIAS = -7        /* the output overlaps an input               */
+    BITDELTA_ERR_ALIAS = -7,       /* the output overlaps an input               */
+    BITDELTA_ERR_TENANT = -8       /* a tenant id is outside [0, T) (reported in
+                                      validation mode only, see bitdelta_matmul) */
 } bitdelta_status;
 
 typedef enum {
@@ -133,12 +135,17 @@ int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base,
  * matrix-core GEMM; the decode-shaped path keeps the two sums apart and
  * never rounds the weight.
  * A row whose tenant id is outside [0, T) is written as quiet NaN (ids live in
- * device memory, so they are not checked on the host).
+ * device memory, so they are not checked on the host).  Validation mode: with
+ * the environment variable BITDELTA_VALIDATE set to a value other than "0",
+ * a batched call first reads the ids back (a device-to-host copy on `stream`
+ * and a synchronisation of `stream`, so not under graph capture) and returns
+ * BITDELTA_ERR_TENANT, launching nothing, if any id is outside [0, T); a
+ * failure of that read-back returns BITDELTA_ERR_HIP.  Meant for debugging.
  * M == 0 or N == 0 is a no-op; K == 0 writes zeros.
  * Batched requests with M >= 256, K a multiple of 64 and T <= 2048 run one
  * fused GEMM per tenant over that tenant's rows (grouped on the device);
  * other batched requests with M > 64 are served 64 rows at a time.
- * Errors: NULL, SHAPE, ALIGN, DTYPE, ALIAS, HIP.
+ * Errors: NULL, SHAPE, ALIGN, DTYPE, ALIAS, HIP; TENANT in validation mode.
  */
 int bitdelta_matmul(const uint16_t* x, int64_t M, int64_t K,
                     const uint16_t* w_base, int64_t N,

@@ -60,6 +60,28 @@ int check_matmul(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w, int
     return BITDELTA_OK;
 }
 
+// Validation mode (BITDELTA_VALIDATE set and not "0"): read the tenant ids back
+// through a fixed host buffer, in chunks, and report any id outside [0, T).
+bool validation_mode() {
+    const char* v = getenv("BITDELTA_VALIDATE");
+    return v != nullptr && v[0] != '\0' && strcmp(v, "0") != 0;
+}
+
+int check_tenant_ids(const int32_t* ids, int64_t M, int32_t T, hipStream_t stream) {
+    constexpr int64_t kChunk = 1024;
+    int32_t buf[kChunk];
+    for (int64_t off = 0; off < M; off += kChunk) {
+        const int64_t n = M - off < kChunk ? M - off : kChunk;
+        if (hipMemcpyAsync(buf, ids + off, (size_t)n * sizeof(int32_t), hipMemcpyDeviceToHost, stream) !=
+                hipSuccess ||
+            hipStreamSynchronize(stream) != hipSuccess)
+            return BITDELTA_ERR_HIP;
+        for (int64_t i = 0; i < n; ++i)
+            if (buf[i] < 0 || buf[i] >= T) return BITDELTA_ERR_TENANT;
+    }
+    return BITDELTA_OK;
+}
+
 int choose_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
     if (M <= kSkinnyRows) return BITDELTA_PATH_SKINNY;
     if (!has_tenant_ids) return BITDELTA_PATH_PREFILL;
@@ -85,6 +107,7 @@ const char* bitdelta_status_string(int status) {
         case BITDELTA_ERR_UNSUPPORTED: return "request not supported by the selected path";
         case BITDELTA_ERR_HIP: return "HIP runtime error at launch";
         case BITDELTA_ERR_ALIAS: return "output overlaps an input";
+        case BITDELTA_ERR_TENANT: return "a tenant id is outside [0, T) (validation mode)";
         default: return "unknown status";
     }
 }
@@ -156,6 +179,10 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_
         !bitdelta::prefill_grouped_supported((int)M, (int)N, (int)K, T))
         return BITDELTA_ERR_UNSUPPORTED;
     if (M == 0 || N == 0) return BITDELTA_OK;
+    if (tenant_ids != nullptr && validation_mode()) {
+        rc = check_tenant_ids(tenant_ids, M, T, stream);
+        if (rc != BITDELTA_OK) return rc;
+    }
     const int et = in_dtype;
 
     if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr)

@@ -42,7 +42,7 @@ def test_no_oracle_symbols_in_library():
 
 def test_version_and_status_strings(lib):
     assert lib.bitdelta_version() >= 100
-    for code in range(-7, 1):
+    for code in range(-8, 1):
         s = bd.status_string(code)
         assert s and s != "unknown status"
     assert bd.status_string(-99) == "unknown status"

@@ -137,3 +137,33 @@ def test_batched_f16():
     ref = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids, dtype="f16")
     relf, _ = check(y, ref, p.x, p.w, p.alpha, p.tenant_ids, dtype="f16")
     assert relf < 1e-5, relf
+
+
+@pytest.mark.parametrize("M,K", [(40, 512), (8, 256), (300, 128)])
+def test_validation_mode_rejects_out_of_range_ids(M, K, monkeypatch):
+    # BITDELTA_VALIDATE=1: the ids are read back before any launch; an id outside
+    # [0, T) returns the tenant status and leaves the output untouched
+    import paper_2609_36800_amd as bd
+    t = torch()
+    N, T = 48, 5
+    p = wl.make_problem(M, N, K, T, seed=M + K + 3, multi_tenant=True, y_dtype="f32")
+    tid = p.tenant_ids.copy()
+    tid[M // 2] = T
+    args = (dev_half(p.x, "bf16"), dev_half(p.w, "bf16"), dev_words(p.packed), dev_f32(p.alpha))
+    monkeypatch.setenv("BITDELTA_VALIDATE", "1")
+    log(f"validation mode M={M} K={K}")
+    y = t.full((M, N), 7.0, dtype=t.float32, device="cuda")
+    with pytest.raises(bd.BitDeltaError) as e:
+        bd.matmul(*args, tenant_ids=dev_i32(tid), out=y)
+    assert e.value.status == -8
+    t.cuda.synchronize()
+    assert bool((y == 7.0).all())
+    # valid ids in validation mode: the same result as without it
+    y1 = bd.matmul(*args, tenant_ids=dev_i32(p.tenant_ids), out_dtype=t.float32)
+    monkeypatch.setenv("BITDELTA_VALIDATE", "0")
+    y0 = bd.matmul(*args, tenant_ids=dev_i32(p.tenant_ids), out_dtype=t.float32)
+    t.cuda.synchronize()
+    assert t.equal(y0, y1)
+    relf, _ = check(host_out(y1), oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    if M <= 64:     # decode-shaped paths never round the effective weight
+        assert relf < 1e-5, relf
