@@ -150,7 +150,7 @@ struct Copier {
     }
     __device__ __forceinline__ void issue_w(int tt) const {
         const int tc = min(tt, KT - 1);
-        copy16_to_lds(wsrc + (size_t)tc * kTileK, lds + L::kWOff + (tt % NWR) * L::kW + cw * 1024);
+        copy16_to_lds_nt(wsrc + (size_t)tc * kTileK, lds + L::kWOff + (tt % NWR) * L::kW + cw * 1024);
     }
     // half h of super-tile s
     __device__ __forceinline__ void issue_s(int s, int h) const {

@@ -217,7 +217,7 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
         for (int i = 0; i < per_wave; ++i) {
             const int q = min(wv + i * kWaves, nq - 1);       // surplus copies repeat the last one
             const int chunk = min(4 * q + (lane >> 4), KW / 4 - 1);
-            copy16_to_lds(srow + 4 * chunk, sg + q * 1024);
+            copy16_to_lds_nt(srow + 4 * chunk, sg + q * 1024);
         }
     }
 
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
         const int tc = min(tt, KT - 1);                       // tail tiles repeat the last one
         char* buf = ring + (tt % NB) * C::kTileBytes;
         const int kbw = min(tc * kTileBlocks + (wchunk >> 2), KB - 1);
-        copy16_to_lds(wsrc + (size_t)kbw * 32 + 8 * (wchunk & 3), buf + wv * 1024);
+        copy16_to_lds_nt(wsrc + (size_t)kbw * 32 + 8 * (wchunk & 3), buf + wv * 1024);
         if (!XUP && lane < C::kXLanes) {
             const int kbx = min(tc * kTileBlocks + (xchunk >> 2), KB - 1);
             copy16_to_lds(xsrc + (size_t)kbx * 32 + 8 * (xchunk & 3),

@@ -175,7 +175,8 @@ __global__ __launch_bounds__(kWaves * 64, 2) void multi_kernel(
                 char* buf = ring + (tt % NB) * C::kTileBytes;
                 // later passes re-read a fixed W tile (cached) to keep the copy count
                 const int kb_w = first_pass ? min(tc * kTileBlocks + wkb, KB - 1) : 0;
-                copy16_to_lds(wsrc + (size_t)kb_w * 32, buf + wv * 1024);
+                if (first_pass) copy16_to_lds_nt(wsrc + (size_t)kb_w * 32, buf + wv * 1024);
+                else copy16_to_lds(wsrc + (size_t)kb_w * 32, buf + wv * 1024);
                 const int kw0 = min(tc * kTileBlocks, KW - 4);       // K is a multiple of 128
 #pragma unroll
                 for (int j = 0; j < C::kSOps; ++j) {
