@@ -303,6 +303,18 @@ def context_ceilings(dev, warmup):
     return out
 
 
+def cpu_model() -> str:
+    """The host CPU's model name as the kernel reports it (empty if unknown)."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
 def cpu_baseline(budget_s: float):
     """fp64 oracle timed on the headline workload (the M = 1 and M = 16 pair
     against one 4096x4096 matrix), repeated until about budget_s seconds."""
@@ -320,7 +332,7 @@ def cpu_baseline(budget_s: float):
         secs += time.perf_counter() - t0
         reps += 1
     return {"value": reps * b / secs / 1e12, "unit": "TB/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
+            "kind": "oracle", "host_cpus": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
             "sample": f"full decode pair (M=1 and M=16, N=K=4096, {b} algorithmic bytes per "
                       f"pass), {reps} passes in {secs:.2f} s, fp64 with OpenMP over features",
             "seconds": secs}
