@@ -243,13 +243,14 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
     const int xidx = wv * C::kXLanes + lane;                  // chunk index inside the x tile
     const int xr = xidx >> 5, xchunk = tswz(xr, xidx & 31);
     const uint16_t* xsrc = x + (size_t)min(xr, M - 1) * K;
+    // Tiles past the end are never issued: the last D tiles run in an unrolled
+    // tail whose waits leave only the real tiles after them in flight.
     auto issue_tile = [&](int tt) {
-        const int tc = min(tt, KT - 1);                       // tail tiles repeat the last one
         char* buf = ring + (tt % NB) * C::kTileBytes;
-        const int kbw = min(tc * kTileBlocks + (wchunk >> 2), KB - 1);
+        const int kbw = min(tt * kTileBlocks + (wchunk >> 2), KB - 1);
         copy16_to_lds_nt(wsrc + (size_t)kbw * 32 + 8 * (wchunk & 3), buf + wv * 1024);
         if (!XUP && lane < C::kXLanes) {
-            const int kbx = min(tc * kTileBlocks + (xchunk >> 2), KB - 1);
+            const int kbx = min(tt * kTileBlocks + (xchunk >> 2), KB - 1);
             copy16_to_lds(xsrc + (size_t)kbx * 32 + 8 * (xchunk & 3),
                           buf + C::kWBytes + wv * (C::kXLanes * 16));
         }
@@ -261,13 +262,7 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
     const int xrow = min(nl, XR - 1);
     const int xoff = C::kWBytes + xrow * kTileRow + 16 * tswz(xrow, c);
     f32x4 accb = {0.f, 0.f, 0.f, 0.f}, accs = {0.f, 0.f, 0.f, 0.f};
-
-#pragma unroll
-    for (int i = 0; i < D; ++i) issue_tile(i);
-    for (int t = 0; t < KT; ++t) {
-        wait_vm_lgkm0<(D - 1) * C::kOpsPerTile>();
-        raw_barrier();
-        issue_tile(t + D);              // into the buffer of tile t-1, free after the barrier
+    auto compute = [&](int t) {
         const int kb = t * kTileBlocks + wv;
         if (kb < KB) {
             const char* buf = ring + (t % NB) * C::kTileBytes;
@@ -279,7 +274,28 @@ __global__ __launch_bounds__(kWaves * 64) void stream_decode_kernel(
             accb = mfma16<ET>(xa, bw, accb);
             accs = mfma16<ET>(xa, decode_signs8<ET>(sb), accs);
         }
+    };
+
+#pragma unroll
+    for (int i = 0; i < D; ++i)
+        if (i < KT) issue_tile(i);
+    // tile t's copies are waited for with the D-1 later tiles left in flight
+    for (int t = 0; t < KT - D; ++t) {
+        wait_vm_lgkm0<(D - 1) * C::kOpsPerTile>();
+        raw_barrier();
+        issue_tile(t + D);              // into the buffer of tile t-1, free after the barrier
+        compute(t);
     }
+    // the last D tiles: tile KT-D+i has D-1-i real tiles after it in flight
+    static_for<D>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const int t = KT - D + i;
+        if (t >= 0) {
+            wait_vm_lgkm0<(D - 1 - i) * C::kOpsPerTile>();
+            raw_barrier();
+            compute(t);
+        }
+    });
     wait_vm_lgkm0<0>();
     __syncthreads();
 
