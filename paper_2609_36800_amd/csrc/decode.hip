@@ -175,9 +175,10 @@ struct StreamCfg {
     static constexpr int kWBytes = kFeat * kTileRow;          // W: 16 rows x 512 B
     static constexpr int kXBytes = XUP ? 0 : XR * kTileRow;   // x: XR rows x 512 B per tile
     static constexpr int kTileBytes = kWBytes + kXBytes;
-    // ring depth (tiles): with x copied per tile (16 rows) a 4-deep ring measured
-    // ~3% faster than 6 (and 8 slower still); with x up front 6 beat 4, 10 and 14
-    static constexpr int kNB = (XR == 16 && !XUP) ? 4 : 6;
+    // ring depth (tiles): 6 measured best with x copied per tile (16 rows: 8.77 us
+    // at 4096x4096 against 8.86 for 5 and 9.0 for 4) and level with 8 with x up
+    // front (4, 5 and 10 slower)
+    static constexpr int kNB = 6;
     static constexpr int kRing = kNB * kTileBytes;
     static constexpr int kOpsPerTile = XUP ? 1 : 2;           // copies per wave per tile
     static constexpr int kXLanes = XR * 4;                    // lanes of a wave copying x
