@@ -338,14 +338,28 @@ def cpu_baseline(budget_s: float):
             "seconds": secs}
 
 
-def kernel_source_hash():
-    """Hash of the dominant kernel's source: a recorded traffic figure is only
-    valid for the kernel it was measured on."""
+def code_text(src: str) -> str:
+    """C/C++ source without comments and with whitespace runs collapsed, so
+    that editing a comment does not change the hash of the code."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
+def kernel_source_hash(read=None):
+    """Hash of the dominant kernel's code (comments excluded): a recorded
+    traffic figure is only valid for the kernel it was measured on.  `read`
+    maps a file name to its text (default: the files in this tree)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("decode.hip", "device.h"):
-        with open(os.path.join(ROOT, "paper_2609_36800_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+    for f in ("decode.hip", "device.h", "ldscopy.h"):
+        if read is None:
+            with open(os.path.join(ROOT, "paper_2609_36800_amd", "csrc", f)) as fh:
+                text = fh.read()
+        else:
+            text = read(f)
+        h.update(code_text(text).encode())
     return h.hexdigest()[:16]
 
 

@@ -165,6 +165,9 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(
 // cache line (the register path above issues 64-byte half lines), and the
 // streaming does not depend on how many waves are resident.  In tile t wave w
 // computes k-block 8t + w from LDS; one vmcnt wait plus one barrier per tile.
+// W and the sign rows are read once per launch and copied with the
+// non-temporal hint; x, shared by every workgroup through L2, is not.  The
+// ring stops at the last tile of K (no repeat copies to drain at the end).
 // ---------------------------------------------------------------------------
 constexpr int kTileBlocks = 8;                  // k-blocks per tile (one per wave)
 constexpr int kTileRow = kTileBlocks * 64;      // bytes of one row segment of a tile
