@@ -40,9 +40,10 @@ hipError_t launch_multi(const uint16_t* x, int M, int K, const uint16_t* w, int 
                         int T, void* y, int y_dtype, int et, hipStream_t stream);
 
 // Batched matmul for up to 64 rows and at most 16 distinct tenants, K a
-// multiple of 256: each tenant's rows gathered into 16-row fragments, one sign
+// multiple of 128: each tenant's rows gathered into 16-row fragments, one sign
 // decode per tenant and k-block.  batched_supported says where the dispatcher
-// uses it (33 to 64 rows, and 17 to 32 rows when N <= 4096).
+// uses it (17 to 64 rows when N <= 4096 and K is a multiple of 256; above
+// 4096 features also 8 to 16 rows over at most 8 tenants).
 bool batched_supported(int M, int N, int K, int T);
 hipError_t launch_batched(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                           const uint32_t* packed, const float* alpha, const int32_t* tenant_ids,

@@ -1,11 +1,14 @@
 """Parity of the batched decode-shaped kernels with the fp64 oracle.
 
-Batched requests with 33 to 64 rows (and 17 to 32 rows when the grid is one
-workgroup per CU, at most 4096 features), at most 16 distinct
-tenants and K a multiple of 256 take the kernel that gathers each tenant's rows
-into 16-row fragments (one sign decode per tenant and k-block); other requests
-take the tenant-slot kernel.  Cases cover the 32-row and 64-row forms and both
-tenant-slot configurations of each (up to 8 and up to 16 tenants), tenant ids
+Batched requests with at most 16 distinct tenants take the kernel that
+gathers each tenant's rows into 16-row fragments (one sign decode per tenant
+and k-block): at most 4096 features, 17 to 64 rows and K a multiple of 256
+(8-wave workgroups, one per CU); above 4096 features, 17 to 64 rows, or 8 to
+16 rows over at most 8 tenants, K a multiple of 128 (4-wave workgroups, two or
+three per CU; 33 to 64 rows over more than 8 tenants keep 8 waves).  Other
+requests take the tenant-slot kernel.  Cases cover the 32-row and 64-row forms
+of both workgroup sizes and both tenant-slot configurations of each (up to 8
+and up to 16 tenants), tenant ids
 used directly as sign slots (at most that many tenants) and compacted (more),
 a K that ends inside a 1024-k sign super-tile, more row fragments than one pass
 holds, out-of-range ids, the exact decode-isolating forms, fp16 and run-to-run
@@ -36,6 +39,10 @@ CASES = [  # M, N, K, T
     (36, 40, 11008, 4), (64, 33, 1280, 12), (64, 20, 512, 64),
     (17, 60, 1024, 12), (24, 50, 2304, 5), (32, 70, 4096, 8), (32, 40, 512, 40),
     (20, 4096, 512, 10), (20, 4112, 512, 10),
+    # above 4096 features: 4-wave workgroups, 128-k tiles
+    (64, 4200, 640, 8), (40, 4112, 1152, 3), (33, 4128, 128, 8), (48, 4160, 512, 16),
+    (32, 4112, 640, 8), (24, 4200, 896, 16), (17, 4128, 128, 12), (32, 4144, 384, 40),
+    (16, 4112, 768, 8), (8, 4112, 384, 5), (12, 4112, 512, 12), (64, 4112, 384, 12),
 ]
 
 
@@ -58,12 +65,15 @@ def test_batched_ragged(M, N, K, T, yd):
     (32, 16, [1] * 15 + [17]),          # 15 + 2 = 17 fragments: two passes of 16
     (32, 16, [2] * 16),                 # 16 fragments of 2 rows
     (32, 8, [32] + [0] * 7),            # one tenant, two fragments
+    (16, 8, [2] * 8),                   # 8 fragments of 2 rows
+    (16, 8, [16] + [0] * 7),            # one tenant, one fragment
 ])
-def test_batched_fragment_layouts(M, T, counts):
-    p = wl.make_problem(M, 60, 1024, T, seed=M + T + len(counts), multi_tenant=True, y_dtype="f32")
+@pytest.mark.parametrize("N,K", [(60, 1024), (4112, 768)])
+def test_batched_fragment_layouts(M, T, counts, N, K):
+    p = wl.make_problem(M, N, K, T, seed=M + T + len(counts), multi_tenant=True, y_dtype="f32")
     ids = np.repeat(np.arange(T), counts).astype(np.int32)
     p.tenant_ids = np.random.default_rng(sum(counts[:3])).permutation(ids)
-    log(f"batched fragments M={M} T={T} counts={counts}")
+    log(f"batched fragments M={M} N={N} K={K} T={T} counts={counts}")
     y = host_out(run_matmul(p, path=SKINNY))
     relf, _ = check(y, oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
     assert relf < 1e-5, relf
@@ -117,9 +127,10 @@ def test_batched_one_hot_rows_every_bit_position():
         np.testing.assert_allclose(y, ref, rtol=2.0 ** -23, atol=0)
 
 
-def test_batched_deterministic():
-    p = wl.make_problem(64, 300, 4096, 8, seed=33, multi_tenant=True, y_dtype="bf16")
-    log("batched determinism")
+@pytest.mark.parametrize("M,N", [(64, 300), (64, 4400), (32, 4400)])
+def test_batched_deterministic(M, N):
+    p = wl.make_problem(M, N, 4096, 8, seed=33, multi_tenant=True, y_dtype="bf16")
+    log(f"batched determinism M={M} N={N}")
     y1 = run_matmul(p, path=SKINNY).view(torch().int16).cpu().numpy()
     y2 = run_matmul(p, path=SKINNY).view(torch().int16).cpu().numpy()
     assert np.array_equal(y1, y2)

@@ -1,8 +1,9 @@
 """Parity of the tenant-slot batched kernel (multi_kernel) with the fp64 oracle.
 
 The dispatcher sends it batched requests with K a multiple of 128 that the
-gathered-fragment kernel does not take: up to 16 rows, 17 to 32 rows with more
-than 4096 features, K not a multiple of 256, or more than 16 distinct tenants.
+gathered-fragment kernel does not take: up to 16 rows (up to 7 rows, or more
+than 8 tenants, above 4096 features), K not a multiple of 256 at most 4096
+features, or more than 16 distinct tenants.
 The cases cover every (row fragments, staged slots) configuration (1 to 4
 fragments of 16 rows; 4, 8 or 16 slots), K from one 128-k tile up to a few
 dozen, more than 4096 features, several passes over the tenants, out-of-range
@@ -25,7 +26,9 @@ CASES = [  # M, N, K, T: (row fragments MB, staged slots P)
     (8, 70, 640, 7),        # MB 1, P 8
     (16, 50, 1152, 16),     # MB 1, P 16, K = 9 tiles
     (32, 60, 640, 16),      # MB 2, P 16 (K not a multiple of 256)
-    (24, 4112, 384, 9),     # MB 2, more than 4096 features
+    (24, 4112, 384, 20),    # MB 2, more than 4096 features and 16 tenants
+    (12, 4112, 640, 9),     # MB 1, more than 4096 features, 9 tenants
+    (7, 4160, 384, 3),      # MB 1, more than 4096 features, 7 rows
     (20, 40, 128, 2),       # MB 2, P 4, one tile
     (40, 50, 896, 8),       # MB 3, P 8
     (48, 30, 128, 5),       # MB 3, P 8, one tile
