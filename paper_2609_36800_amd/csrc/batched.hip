@@ -21,8 +21,10 @@
 // every workgroup computes the routing (wave 0, ballots) and enters the loop
 // specialised for its F.  Sign slot u holds tenant u when there are at most
 // as many tenants as slots, so the first tiles' copies go out before the
-// routing is known; with more tenants the slots are compacted to the tenants
-// present and the copies wait for the routing.
+// routing is known (after it, the slots of tenants without rows are filled
+// from a present tenant's rows, which L2 already holds); with more tenants the
+// slots are compacted to the tenants present and the copies wait for the
+// routing.
 //
 // Memory path.  A workgroup of WV waves (8 or 4) owns 16 output features; K
 // runs in 32*WV-k tiles and wave w computes k-block w of every tile.  All
@@ -385,7 +387,13 @@ __global__ __launch_bounds__(WV * 64, (waves_per_simd<XR, UMAX, NWR, NXR, WV>())
             if ((rank & 15) == 0) rt.frag_slot[fidx] = slot;
             if (!ident && rank == 0 && slot < 16) rt.slot_tenant[slot] = (int)kp;
         }
-        if (ident && lane < T) rt.slot_tenant[lane] = lane;
+        if (ident) {
+            // slot u holds tenant u; the slots of tenants without rows (never
+            // read) copy the first present tenant's rows instead, from L2
+            const uint32_t k0 = __builtin_amdgcn_readfirstlane(kp);
+            if (lane < T) rt.slot_tenant[lane] = k0 < kKeyInvalid ? (int)k0 : 0;
+            if (valid && kp != kprev) rt.slot_tenant[kp] = (int)kp;
+        }
         if (lane == 0) {
             rt.nfrag = __popcll(fstart);
             rt.nslot = ident ? T : __popcll(tstart);
