@@ -383,11 +383,28 @@ def pmc_pass(steps, workload="decode"):
     WRITE_SIZE readings calibrate the counters (known bytes read and written).
     prefill: `steps` launches each of the bf16 and fp16 4096^3 fused GEMM.
     multi: `steps` launches of the batched kernel at 64 rows, 8 tenants,
-    4096x4096, on 12 rotating buffer sets."""
+    4096x4096, on 12 rotating buffer sets.  mtdecode: `steps` launches of the
+    multi-tenant decode workload (32 rows, 16 tenants, 11008x4096) on 4
+    rotating buffer sets, with the distinct tenants of each set printed."""
     import torch
     import paper_2609_36800_amd as bd
     dev = torch.device("cuda:0")
     launcher = Launcher(bd.load_library())
+    if workload == "mtdecode":
+        calls, keep, distinct = [], [], []
+        for r in range(4):
+            d = make_sets(1, 32, 11008, 4096, 16, True, 21 + r, dev)[0]
+            y = torch.empty((32, 11008), dtype=torch.bfloat16, device=dev)
+            keep.append((d, y))
+            distinct.append(int(torch.unique(d["tenant_ids"]).numel()))
+            calls.append(launcher.matmul(d["x"], d["w"], d["packed"], d["alpha"],
+                                         d["tenant_ids"], y))
+        for i in range(steps):
+            calls[i % len(calls)]()
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_pass": workload, "launches": steps, "distinct_tenants": distinct}),
+              flush=True)
+        return
     if workload in ("prefill", "multi"):
         calls, keep = [], []
         if workload == "prefill":
@@ -492,7 +509,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only launch the headline kernels and a calibration copy (for rocprofv3 --pmc)")
-    ap.add_argument("--pmc-workload", choices=("decode", "prefill", "multi"), default="decode",
+    ap.add_argument("--pmc-workload", choices=("decode", "prefill", "multi", "mtdecode"), default="decode",
                     help="what --pmc-pass launches")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic record from two --pmc runs of --pmc-pass (no GPU needed)")
