@@ -42,10 +42,10 @@
 // covers every earlier sign part while the deeper W ring stays in flight, and
 // one barrier per tile publishes the tile.
 //
-// Occupancy.  The 8-wave configurations take 130 to 155 KB of LDS, one
+// Occupancy.  The 8-wave configurations take 133 to 157 KB of LDS, one
 // workgroup per CU: with at most 256 workgroups (N <= 4096) the whole grid is
 // resident at once and each workgroup's eight waves split K finely.  Larger
-// grids run in rounds; there the 4-wave configurations (46 to 67 KB) hold two
+// grids run in rounds; there the 4-wave configurations (49 to 69 KB) hold two
 // or three workgroups per CU, so one workgroup's waits and barriers overlap
 // another's copies and products, and the last round is shorter.
 //
@@ -90,7 +90,7 @@ __device__ __forceinline__ int swz16(int row, int chunk) { return chunk ^ (row &
 struct Routing {
     int tenant_of_row[kRowsMax];          // -1: id out of range
     int frag_of_row[kRowsMax];            // fragment holding row m, -1: none
-    int8_t frag_row[kRowsMax][16];        // row in slot i of fragment f, -1: empty
+    int frag_row[kRowsMax][16];           // row in slot i of fragment f, -1: empty
     int frag_slot[kRowsMax];              // sign slot (distinct-tenant index) of fragment f
     int slot_tenant[16];                  // tenant of sign slot u
     uint32_t key_sorted[kRowsMax];
@@ -382,7 +382,7 @@ __global__ __launch_bounds__(WV * 64, (waves_per_simd<XR, UMAX, NWR, NXR, WV>())
         const unsigned long long fstart = __ballot(valid && (rank & 15) == 0);
         const int fidx = __popcll(fstart & upto) - 1;
         if (valid) {
-            rt.frag_row[fidx][rank & 15] = (int8_t)rt.sorted_row[p];
+            rt.frag_row[fidx][rank & 15] = rt.sorted_row[p];
             rt.frag_of_row[rt.sorted_row[p]] = fidx;
             if ((rank & 15) == 0) rt.frag_slot[fidx] = slot;
             if (!ident && rank == 0 && slot < 16) rt.slot_tenant[slot] = (int)kp;
@@ -469,14 +469,14 @@ hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
     return launch_cfg<ET, XR, U, NW, NX, WV>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, stream)
     if (M <= 32) {
         if (rounds) {
-            if (few) BD_CFG(32, 8, 3, 2, 4);        // 46 KB LDS, 164 VGPRs: three per CU
-            BD_CFG(32, 16, 4, 2, 4);                // 66 KB: two per CU
+            if (few) BD_CFG(32, 8, 3, 2, 4);        // 49 KB LDS, 163 VGPRs: three per CU
+            BD_CFG(32, 16, 4, 2, 4);                // 69 KB: two per CU
         }
         if (few) BD_CFG(32, 8, 4, 4, 8);            // 133 KB: 4% faster than 3-deep rings
         BD_CFG(32, 16, 3, 3, 8);
     }
     if (few) {
-        if (rounds) BD_CFG(64, 8, 4, 2, 4);         // 66 KB: two per CU
+        if (rounds) BD_CFG(64, 8, 4, 2, 4);         // 69 KB: two per CU
         BD_CFG(64, 8, 3, 3, 8);
     }
     BD_CFG(64, 16, 3, 2, 8);
