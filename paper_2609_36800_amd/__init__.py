@@ -110,11 +110,22 @@ def _dev(t, name, dtypes):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _shape(t, shape, name):
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
 def pack(signs, out=None):
     """Pack signs [rows, K] (float32 / bfloat16 / float16 / int8) into int32 words [rows, K/32]."""
     import torch
-    _dev(signs, "signs", (torch.float32, torch.bfloat16, torch.float16, torch.int8))
+    if signs.dim() != 2:
+        raise ValueError(f"signs must be [rows, K], got shape {tuple(signs.shape)}")
     rows, K = signs.shape
+    if K % 32:
+        raise ValueError(f"K = {K} is not a multiple of 32")
+    if out is not None:
+        _shape(out, (rows, K // 32), "out")
+    _dev(signs, "signs", (torch.float32, torch.bfloat16, torch.float16, torch.int8))
     if out is None:
         out = torch.empty((rows, K // 32), dtype=torch.int32, device=signs.device)
     _dev(out, "out", (torch.int32,))
@@ -127,8 +138,14 @@ def unpack(packed, K: int, dtype=None, out=None):
     """Decode int32 words [rows, K/32] into [rows, K] of +1 / -1 (float32 by default)."""
     import torch
     dtype = dtype or torch.float32
-    _dev(packed, "packed", (torch.int32,))
+    if packed.dim() != 2:
+        raise ValueError(f"packed must be [rows, K/32], got shape {tuple(packed.shape)}")
     rows = packed.shape[0]
+    if K % 32 or packed.shape[1] * 32 != K:
+        raise ValueError(f"packed has {packed.shape[1]} words per row; K = {K} needs K/32")
+    if out is not None:
+        _shape(out, (rows, K), "out")
+    _dev(packed, "packed", (torch.int32,))
     if out is None:
         out = torch.empty((rows, K), dtype=dtype, device=packed.device)
     _dev(out, "out", (torch.float32, torch.bfloat16, torch.float16, torch.int8))
@@ -145,11 +162,13 @@ def compress(w_fine, w_base, with_alpha: bool = True):
     scale mean|w_fine - w_base|, and the per-row sums of |w_fine - w_base|.
     """
     import torch
-    _dev(w_fine, "w_fine", (torch.bfloat16, torch.float16))
-    _dev(w_base, "w_base", (w_fine.dtype,))
     if w_fine.shape != w_base.shape or w_fine.dim() != 2:
         raise ValueError("w_fine and w_base must be [rows, K] of the same shape")
     rows, K = w_fine.shape
+    if K % 32:
+        raise ValueError(f"K = {K} is not a multiple of 32")
+    _dev(w_fine, "w_fine", (torch.bfloat16, torch.float16))
+    _dev(w_base, "w_base", (w_fine.dtype,))
     packed = torch.empty((rows, K // 32), dtype=torch.int32, device=w_fine.device)
     row_abs = torch.empty((rows,), dtype=torch.float32, device=w_fine.device)
     alpha = torch.empty((1,), dtype=torch.float32, device=w_fine.device) if with_alpha else None
@@ -166,27 +185,33 @@ def matmul(x, w_base, packed_s, alpha, tenant_ids=None, out_dtype=None, out=None
 
     x [M, K] and w_base [N, K] both bfloat16 or both float16, packed_s int32
     [T, N, K/32] (or [N, K/32]), alpha fp32 [T], tenant_ids int32 [M] or None,
-    out_dtype float32 or the input type (the default).
+    out_dtype float32 or the input type (the default); out, if given, [M, N].
+    Every shape is checked before anything reaches the library, which sees
+    only raw pointers.
     """
     import torch
-    _dev(x, "x", (torch.bfloat16, torch.float16))
-    _dev(w_base, "w_base", (x.dtype,))
-    out_dtype = out_dtype or x.dtype
-    _dev(packed_s, "packed_s", (torch.int32,))
-    _dev(alpha, "alpha", (torch.float32,))
+    if x.dim() != 2 or w_base.dim() != 2 or alpha.dim() != 1 or packed_s.dim() not in (2, 3):
+        raise ValueError("x and w_base must be 2-D, alpha 1-D, packed_s 2-D or 3-D")
     M, K = x.shape
     N = w_base.shape[0]
     T = alpha.numel()
     if packed_s.dim() == 2:
         packed_s = packed_s.unsqueeze(0)
-    if tuple(packed_s.shape) != (T, N, K // 32) or w_base.shape[1] != K:
+    if K % 32 or tuple(packed_s.shape) != (T, N, K // 32) or w_base.shape[1] != K:
         raise ValueError(f"shape mismatch: x {tuple(x.shape)}, w {tuple(w_base.shape)}, "
                          f"packed {tuple(packed_s.shape)}, alpha {T}")
+    if tenant_ids is not None and (tenant_ids.dim() != 1 or tenant_ids.numel() != M):
+        raise ValueError("tenant_ids needs one entry per row")
+    if out is not None:
+        _shape(out, (M, N), "out")
+    _dev(x, "x", (torch.bfloat16, torch.float16))
+    _dev(w_base, "w_base", (x.dtype,))
+    out_dtype = out_dtype or x.dtype
+    _dev(packed_s, "packed_s", (torch.int32,))
+    _dev(alpha, "alpha", (torch.float32,))
     tptr = None
     if tenant_ids is not None:
         _dev(tenant_ids, "tenant_ids", (torch.int32,))
-        if tenant_ids.numel() != M:
-            raise ValueError("tenant_ids needs one entry per row")
         tptr = tenant_ids.data_ptr()
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=x.device)

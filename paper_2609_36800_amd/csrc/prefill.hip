@@ -14,8 +14,9 @@
 // workgroup (4 waves, 2x2) owns a 256x256 output tile, each wave 128x128 =
 // 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane).  Per
 // 64-wide k-tile:
-//   * the x tile is copied global -> LDS by the DMA path (no VGPR staging),
-//     one tile ahead, into one of two LDS buffers;
+//   * the x tile is loaded into registers one tile ahead by buffer loads
+//     (32-bit per-lane offsets, the k offset in a scalar register) and
+//     written to one of two LDS buffers;
 //   * the raw W tile and its sign words are loaded into registers two tiles
 //     ahead (two register sets), and the effective weights of the next tile
 //     are formed and written to the other of two LDS buffers while the

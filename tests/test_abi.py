@@ -182,3 +182,91 @@ def test_path_selection(lib):
     assert bd.matmul_path(4096, 4096, 4096, 8, True) == bd.PATH_PREFILL
     assert bd.matmul_path(4096, 4096, 4000, 8, True) == bd.PATH_SKINNY   # K % 64
     assert bd.matmul_path(4096, 4096, 4096, 2049, True) == bd.PATH_SKINNY
+
+
+# The binding checks every shape before a pointer reaches the library (which
+# sees raw pointers only and cannot tell an undersized buffer): a wrong shape
+# raises ValueError before the device checks, so CPU tensors suffice here.
+
+def _t():
+    import torch
+    return torch
+
+
+def test_binding_matmul_rejects_bad_out_shape():
+    t = _t()
+    x = t.zeros((4, 64), dtype=t.bfloat16)
+    w = t.zeros((8, 64), dtype=t.bfloat16)
+    p = t.zeros((1, 8, 2), dtype=t.int32)
+    a = t.zeros((1,), dtype=t.float32)
+    for shape in [(4, 7), (3, 8), (32,), (4, 8, 1)]:
+        with pytest.raises(ValueError, match="out has shape"):
+            bd.matmul(x, w, p, a, out=t.zeros(shape, dtype=t.bfloat16))
+
+
+def test_binding_matmul_rejects_bad_operand_shapes():
+    t = _t()
+    x = t.zeros((4, 64), dtype=t.bfloat16)
+    w = t.zeros((8, 64), dtype=t.bfloat16)
+    a = t.zeros((2,), dtype=t.float32)
+    with pytest.raises(ValueError, match="shape mismatch"):
+        bd.matmul(x, w, t.zeros((2, 8, 3), dtype=t.int32), a)          # K/32 words
+    with pytest.raises(ValueError, match="shape mismatch"):
+        bd.matmul(x, w, t.zeros((1, 8, 2), dtype=t.int32), a)          # T from alpha
+    with pytest.raises(ValueError, match="shape mismatch"):
+        bd.matmul(x, t.zeros((8, 96), dtype=t.bfloat16), t.zeros((2, 8, 2), dtype=t.int32), a)
+    with pytest.raises(ValueError, match="shape mismatch"):
+        bd.matmul(t.zeros((4, 48), dtype=t.bfloat16), t.zeros((8, 48), dtype=t.bfloat16),
+                  t.zeros((2, 8, 1), dtype=t.int32), a)                 # K % 32
+    with pytest.raises(ValueError, match="one entry per row"):
+        bd.matmul(x, w, t.zeros((2, 8, 2), dtype=t.int32), a, tenant_ids=t.zeros((5,), dtype=t.int32))
+    with pytest.raises(ValueError, match="2-D"):
+        bd.matmul(x[None], w, t.zeros((2, 8, 2), dtype=t.int32), a)
+
+
+def test_binding_pack_unpack_reject_bad_shapes():
+    t = _t()
+    with pytest.raises(ValueError, match="out has shape"):
+        bd.pack(t.zeros((4, 64)), out=t.zeros((4, 1), dtype=t.int32))
+    with pytest.raises(ValueError, match="out has shape"):
+        bd.pack(t.zeros((4, 64)), out=t.zeros((3, 2), dtype=t.int32))
+    with pytest.raises(ValueError, match="multiple of 32"):
+        bd.pack(t.zeros((4, 48)))
+    with pytest.raises(ValueError, match="rows, K"):
+        bd.pack(t.zeros((256,)))
+    packed = t.zeros((4, 2), dtype=t.int32)
+    with pytest.raises(ValueError, match="words per row"):
+        bd.unpack(packed, 96)                 # would read past packed
+    with pytest.raises(ValueError, match="words per row"):
+        bd.unpack(packed, 32)                 # would decode rows wrongly
+    with pytest.raises(ValueError, match="out has shape"):
+        bd.unpack(packed, 64, out=t.zeros((4, 32)))
+    with pytest.raises(ValueError, match="out has shape"):
+        bd.unpack(packed, 64, out=t.zeros((5, 64)))
+
+
+def test_binding_compress_rejects_bad_shapes():
+    t = _t()
+    with pytest.raises(ValueError, match="same shape"):
+        bd.compress(t.zeros((4, 64), dtype=t.bfloat16), t.zeros((4, 32), dtype=t.bfloat16))
+    with pytest.raises(ValueError, match="multiple of 32"):
+        bd.compress(t.zeros((4, 48), dtype=t.bfloat16), t.zeros((4, 48), dtype=t.bfloat16))
+
+
+def test_plain_matmul_entry_host_errors(lib):
+    # bitdelta_matmul itself (automatic path, bf16 inputs): same host checks
+    def pm(x=A, M=4, K=64, w=B, N=8, p=C, alpha=D, tid=None, T=1, y=E, yd=bd.BF16):
+        return lib.bitdelta_matmul(x, M, K, w, N, p, alpha, tid, T, y, yd, None)
+    assert pm(K=48) == -2
+    assert pm(M=-1) == -2
+    assert pm(T=0) == -2
+    assert pm(x=None) == -1
+    assert pm(y=None) == -1
+    assert pm(alpha=None) == -1
+    assert pm(x=A + 2) == -3
+    assert pm(tid=D + 0x1000 + 2) == -3
+    assert pm(yd=bd.I8) == -4
+    assert pm(yd=bd.F16) == -4            # bf16 inputs: a 16-bit output is bf16
+    assert pm(y=B + 64) == -7
+    assert pm(M=0) == 0
+    assert pm(N=0, y=None) == 0
