@@ -55,6 +55,15 @@ def load_library(path: str = LIB_PATH):
         raise RuntimeError(
             f"{path} is missing: build the HIP library first "
             "(python -c 'import __graft_entry__ as g; g.build()')")
+    # The library takes its HIP runtime from whatever libamdhip64 is already
+    # in the process.  torch ships its own copy: load it first, or the process
+    # ends up with two runtimes (torch's, owning the tensors and streams, and
+    # the system one the library would pull in) and launches on torch's
+    # memory fail.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     P, I64, I32, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
     lib.bitdelta_pack.argtypes = [P, I, I64, I64, P, P]

@@ -35,6 +35,11 @@ bool overlaps(const void* a, size_t abytes, const void* b, size_t bbytes) {
 
 int hip_status(hipError_t e) { return e == hipSuccess ? BITDELTA_OK : BITDELTA_ERR_HIP; }
 
+// The launchers report hipGetLastError() after their launches; an error left
+// behind by an earlier, unrelated runtime call of the caller (a not-ready
+// query, say) would otherwise be reported as this call's launch failure.
+void clear_stale_error() { (void)hipGetLastError(); }
+
 // Largest extent any kernel indexes with 32-bit arithmetic.
 constexpr int64_t kMaxDim = (int64_t)1 << 30;
 
@@ -124,6 +129,7 @@ int bitdelta_pack(const void* signs, int in_dtype, int64_t rows, int64_t K, uint
         return BITDELTA_ERR_ALIAS;
     // the sign bit of both 16-bit formats is bit 15: one kernel serves both
     if (in_dtype == BITDELTA_F16) in_dtype = BITDELTA_BF16;
+    clear_stale_error();
     return hip_status(bitdelta::launch_pack(signs, in_dtype, rows * K, packed, stream));
 }
 
@@ -137,6 +143,7 @@ int bitdelta_unpack(const uint32_t* packed, int64_t rows, int64_t K, void* signs
     if (!aligned(signs, 4 * es) || !aligned(packed, 4)) return BITDELTA_ERR_ALIGN;
     if (overlaps(packed, (size_t)rows * (K / 32) * 4, signs, (size_t)rows * K * es))
         return BITDELTA_ERR_ALIAS;
+    clear_stale_error();
     return hip_status(bitdelta::launch_unpack(packed, rows * K, signs, out_dtype, stream));
 }
 
@@ -159,6 +166,7 @@ int bitdelta_compress(const uint16_t* w_fine, const uint16_t* w_base, int64_t ro
         overlaps(alpha, abytes, w_base, wbytes) || overlaps(alpha, abytes, packed, pbytes) ||
         overlaps(alpha, abytes, row_abs_sum, rbytes))
         return BITDELTA_ERR_ALIAS;
+    clear_stale_error();
     return hip_status(bitdelta::launch_compress(w_fine, w_base, (int)rows, (int)K, in_dtype, packed,
                                                 row_abs_sum, alpha, stream));
 }
@@ -184,6 +192,7 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_
         if (rc != BITDELTA_OK) return rc;
     }
     const int et = in_dtype;
+    clear_stale_error();
 
     if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr)
         return hip_status(bitdelta::launch_prefill_grouped(x, (int)M, (int)K, w_base, (int)N,

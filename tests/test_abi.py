@@ -270,3 +270,17 @@ def test_plain_matmul_entry_host_errors(lib):
     assert pm(y=B + 64) == -7
     assert pm(M=0) == 0
     assert pm(N=0, y=None) == 0
+
+
+def test_library_shares_torchs_hip_runtime():
+    # Loading the library before torch must not leave two HIP runtimes in the
+    # process (the library's launches on torch's memory fail if it does).
+    import subprocess
+    import sys
+    code = ("import paper_2609_36800_amd as bd; bd.load_library(); import torch; "
+            "maps = open('/proc/self/maps').read(); "
+            "print(len({l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1", out.stdout
