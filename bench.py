@@ -79,16 +79,19 @@ def make_sets(count, M, N, K, T, multi, seed, dev, prompts=0, dtype="bf16"):
 
 
 def capture(calls, warmup_calls):
-    """Run warmup_calls eagerly, then capture `calls` once into a HIP graph
-    (falls back to eager replay if capture is unavailable)."""
+    """Run warmup_calls eagerly on the capture stream, then capture `calls`
+    once into a HIP graph on it (falls back to eager replay if capture is
+    unavailable).  Warming up on that stream lets the library make its
+    per-stream workspace before capture, where it cannot allocate."""
     import torch
-    for c in warmup_calls:
-        c()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for c in warmup_calls:
+            c()
     torch.cuda.synchronize()
     try:
         g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(s):
             g.capture_begin()
             for c in calls:

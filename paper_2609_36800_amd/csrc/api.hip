@@ -1,8 +1,12 @@
 // C ABI of the binary-delta matmul library: argument checks, path choice and
-// kernel launches.  Everything here runs on the host; nothing is allocated.
+// kernel launches.  Everything here runs on the host.  The only allocation is
+// the grouped prefill's partial-sum workspace, made once per (device, stream)
+// on first need and kept until the process ends.
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+
+#include <mutex>
 
 #include "../../include/bitdelta.h"
 #include "internal.h"
@@ -85,6 +89,45 @@ int check_tenant_ids(const int32_t* ids, int64_t M, int32_t T, hipStream_t strea
             if (buf[i] < 0 || buf[i] >= T) return BITDELTA_ERR_TENANT;
     }
     return BITDELTA_OK;
+}
+
+// Partial-sum workspace of the grouped prefill split, one per (device,
+// stream): two calls on one stream run in order, so they can share it, while
+// calls on different streams may overlap and must not.  Allocated on first
+// need (never while the stream is being captured into a graph: such a call
+// runs without the split) and kept until the process ends.  Every call writes
+// what it reads there, so the contents need no initial value.
+// Allocation failure or a full table also mean "no split", never an error.
+struct Workspace {
+    int device;
+    hipStream_t stream;
+    void* ptr;
+};
+constexpr int kMaxWorkspaces = 64;
+std::mutex g_ws_mutex;
+Workspace g_ws[kMaxWorkspaces];
+int g_ws_count = 0;
+
+void* stream_workspace(hipStream_t stream, size_t bytes) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+    std::lock_guard<std::mutex> lock(g_ws_mutex);
+    for (int i = 0; i < g_ws_count; ++i)
+        if (g_ws[i].device == dev && g_ws[i].stream == stream) return g_ws[i].ptr;
+    if (g_ws_count == kMaxWorkspaces) return nullptr;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) return nullptr;
+    void* p = nullptr;
+    if (hipMalloc(&p, bytes) != hipSuccess) return nullptr;
+    g_ws[g_ws_count++] = {dev, stream, p};
+    return p;
+}
+
+// More output tiles than CUs is possible (the grouped GEMM may split).
+bool grouped_may_split(int64_t M, int64_t N, int32_t T) {
+    const int64_t U = T < M ? T : M;
+    const int64_t tiles_m = (M + 255 * U) / 256, tiles_n = (N + 255) / 256;
+    return tiles_m * tiles_n > 256;
 }
 
 int choose_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids) {
@@ -194,10 +237,18 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_
     const int et = in_dtype;
     clear_stale_error();
 
-    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr)
+    if (path == BITDELTA_PATH_PREFILL && tenant_ids != nullptr) {
+        void* ws = nullptr;
+        size_t ws_bytes = 0;
+        if (grouped_may_split(M, N, T)) {
+            ws_bytes = bitdelta::prefill_split_bytes();
+            ws = stream_workspace(stream, ws_bytes);
+            (void)hipGetLastError();      // a failed allocation only disables the split
+        }
         return hip_status(bitdelta::launch_prefill_grouped(x, (int)M, (int)K, w_base, (int)N,
                                                            packed_s, alpha, tenant_ids, (int)T, y,
-                                                           y_dtype, et, stream));
+                                                           y_dtype, et, stream, ws, ws ? ws_bytes : 0));
+    }
     if (path == BITDELTA_PATH_PREFILL)
         return hip_status(bitdelta::launch_prefill(x, (int)M, (int)K, w_base, (int)N, packed_s,
                                                    alpha, y, y_dtype, et, stream));

@@ -62,11 +62,16 @@ hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, in
                           int et, hipStream_t stream);
 
 // Prefill-shaped batched matmul: one fused GEMM per tenant over its rows,
-// routed on the device; needs prefill_grouped_supported.
+// routed on the device; needs prefill_grouped_supported.  With more than 256
+// output tiles the leftover tiles are split along K over the idle CUs when
+// `scratch` (scratch_bytes, at least prefill_split_bytes() for the full split)
+// can hold their fp32 partial sums and per-tile counters; the counters must be
+// zero on entry and are left zero.  scratch may be null (no split).
+size_t prefill_split_bytes();
 bool prefill_grouped_supported(int M, int N, int K, int T);
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,
                                   const int32_t* tenant_ids, int T, void* y, int y_dtype,
-                                  int et, hipStream_t stream);
+                                  int et, hipStream_t stream, void* scratch, size_t scratch_bytes);
 
 }  // namespace bitdelta

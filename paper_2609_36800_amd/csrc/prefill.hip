@@ -52,6 +52,7 @@ namespace bitdelta {
 namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64;
+constexpr int kCUs = 256;            // MI355X compute units (one output tile each per round)
 constexpr int kThreads = 256;
 constexpr int kChunks = BM * BK / 8 / kThreads;  // 16-byte chunks per thread per operand = 8
 constexpr int kGroupM = 4;
@@ -225,12 +226,40 @@ __device__ __forceinline__ void tile_of(int bid, int tiles_m, int tiles_n, int& 
 // number of tiles is known only on the device, so the grid covers the upper
 // bound and surplus workgroups leave), and collects its tile's row indices.
 constexpr int kMaxGroupedTenants = BM * BK * 2 / (4 * 4);  // 4 histograms of T ints in 32 KB
+constexpr size_t kSplitChunkBytes = (size_t)BM * BN * 4;   // fp32 partial sums of one tile
+constexpr int kSplitVecs = 4 * 4 * 4;                       // f32x4 partials per thread
+constexpr int kSplitMetaInts = BM + 4;                      // row map, column origin, counts
 
-// Returns false (for the whole workgroup) when block `bid` owns no tile;
-// else `tenant`, `tile_n` and rows[0..255] (row index, -1 past the tenant's
-// last row).  hist: 4*T ints of LDS; info: 8 ints of LDS.
+// Work items.  With at most kCUs output tiles (or no room for partial sums)
+// block b takes tile b.  With more tiles, blocks 0 .. kCUs-1 take tiles 0 ..
+// kCUs-1 whole (one round), and the L leftover tiles are split along K into
+// S chunks, S = min(8, k-tiles, room / L, kCUs / L): blocks kCUs + l*S + c
+// take chunk c of leftover tile l, so the second round runs on every CU for
+// 1/S of a tile's time.  A chunk's fp32 partial sums go to `part`; the last
+// chunk of a tile to finish (per-tile counter) adds the S partials in chunk
+// order and writes the tile, so the result does not depend on timing.
+struct WorkItem {
+    int chunk, nchunks, leftover;   // chunk c of nchunks (1: whole tile); leftover tile index
+    int nleft;                      // leftover tiles (split ones)
+};
+
+__device__ __forceinline__ int split_chunks(int ntiles, int room, int KT) {
+    if (ntiles <= kCUs || room <= 0) return 1;
+    const int L = ntiles - kCUs;
+    const int cap = room < kCUs ? room : kCUs;
+    int S = cap / L;
+    S = S < 8 ? S : 8;
+    S = S < KT ? S : KT;
+    return S > 1 ? S : 1;
+}
+
+// Returns false (for the whole workgroup) when block `bid` owns no work;
+// else `tenant`, `tile_n`, the work item and rows[0..255] (row index, -1 past
+// the tenant's last row).  hist: 4*T ints of LDS; info: 8 ints of LDS.
+// room: leftover chunks the partial-sum buffer holds (0: none).
 __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int tiles_n, int bid,
-                           int* hist, int* rows, int* info, int& tenant, int& tile_n) {
+                           int room, int KT, int* split_hdr, int* hist, int* rows, int* info, int& tenant,
+                           int& tile_n, WorkItem& item) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int seg = ((M + 255) >> 8) << 6;  // rows per wave, a multiple of 64
@@ -269,9 +298,27 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
     const int total = info[0] + info[1] + info[2] + info[3];
     int excl = incl - s;
     for (int w2 = 0; w2 < wv; ++w2) excl += info[w2];
-    if (bid >= total * tiles_n) return false;
+    const int ntiles = total * tiles_n;
+    const int S = split_chunks(ntiles, room, KT);
+    // block 0 records this call's split for the reduction launch that follows
+    if (bid == 0 && tid == 0 && split_hdr != nullptr) {
+        split_hdr[0] = S > 1 ? ntiles - kCUs : 0;
+        split_hdr[1] = S;
+    }
+    int tile_idx = bid;
+    item = WorkItem{0, 1, -1, 0};
+    if (S > 1 && bid >= kCUs) {
+        item.nleft = ntiles - kCUs;
+        const int u = bid - kCUs;
+        if (u >= (ntiles - kCUs) * S) return false;
+        item.leftover = u / S;
+        item.chunk = u - item.leftover * S;
+        item.nchunks = S;
+        tile_idx = kCUs + item.leftover;
+    }
+    if (tile_idx >= ntiles) return false;
     int tile_v;
-    tile_of(bid, total, tiles_n, tile_v, tile_n);
+    tile_of(tile_idx, total, tiles_n, tile_v, tile_n);
     if (tile_v >= excl && tile_v < excl + s) {
         int first = excl;
         for (int t = t_beg; t < t_end; ++t) {
@@ -419,13 +466,17 @@ __device__ __forceinline__ uint32_t cvt_pair(f32x2v f) {
 // rows start on 16-byte boundaries (N a multiple of 8 for 16-bit outputs, of 4
 // for fp32), which allows 16-byte stores.
 // GROUPED: the batched form (tenant id per row, at most kMaxGroupedTenants
-// tenants); tiles_m is then the upper bound on the number of row tiles, and
-// tiles_n more workgroups past tiles_m * tiles_n write the rows of invalid ids.
+// tenants); blocks below g_tiles take the work items of route_rows, and
+// tiles_n more blocks past g_tiles write the rows of invalid ids.  part /
+// counters / room: partial-sum buffer (room chunks of 256 KB) and the split
+// record (header of 4 ints, then per leftover tile its row map and column
+// origin) that prefill_reduce_kernel reads; room 0 disables the split.
 template <int ET, int YDT, bool ALIGNED, bool GROUPED>
 __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
     const uint32_t* __restrict__ packed, const float* __restrict__ alpha_p,
-    const int32_t* __restrict__ ids, int T, void* __restrict__ y, int tiles_m, int tiles_n) {
+    const int32_t* __restrict__ ids, int T, void* __restrict__ y, int tiles_m, int tiles_n,
+    float* __restrict__ part, int* __restrict__ counters, int room, int g_tiles) {
     // Two buffers per operand, each [256 rows][64 k] bf16 = 32 KB.
     __shared__ __attribute__((aligned(1024))) uint16_t sA0[BM * BK];
     __shared__ __attribute__((aligned(1024))) uint16_t sA1[BM * BK];
@@ -435,14 +486,21 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     __shared__ int sInfo[GROUPED ? 8 : 1];
 
     int tile_m = 0, tile_n, tenant = 0;
+    WorkItem item{0, 1, -1, 0};
     if constexpr (GROUPED) {
-        if ((int)blockIdx.x >= tiles_m * tiles_n) {
-            write_invalid_rows<ET, YDT>(ids, M, T, N, ((int)blockIdx.x - tiles_m * tiles_n) * BN, y);
+        if ((int)blockIdx.x >= g_tiles) {
+            write_invalid_rows<ET, YDT>(ids, M, T, N, ((int)blockIdx.x - g_tiles) * BN, y);
             return;
         }
-        if (!route_rows(ids, M, T, tiles_n, blockIdx.x, reinterpret_cast<int*>(sA0), sRows, sInfo,
-                        tenant, tile_n))
+        if (!route_rows(ids, M, T, tiles_n, blockIdx.x, room, K / BK, counters, reinterpret_cast<int*>(sA0),
+                        sRows, sInfo, tenant, tile_n, item))
             return;
+        // the chunk is needed again only after the k-loop: keep it in LDS, not
+        // in registers across the loop (sInfo[6], [7] are free after routing)
+        if (threadIdx.x == 0) {
+            sInfo[6] = item.leftover * item.nchunks + item.chunk;
+            sInfo[7] = item.nchunks;
+        }
     } else {
         tile_of(blockIdx.x, tiles_m, tiles_n, tile_m, tile_n);
     }
@@ -461,7 +519,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wm = wv >> 1, wn = wv & 1;
-    const int KT = K / BK;
+    // k-tiles of this work item: all of K, or chunk c of a split leftover tile
+    const int kb0 = item.chunk * (K / BK) / item.nchunks;
+    const int KT = (item.chunk + 1) * (K / BK) / item.nchunks - kb0;
     const int KW = K >> 5;
     const float neg_alpha = -alpha_p[tenant];
     const uint32_t neg_alpha_h = to_f16(neg_alpha) | ((uint32_t)to_f16(neg_alpha) << 16);
@@ -485,9 +545,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         if constexpr (GROUPED) xr = (uint32_t)(sRows[r] >= 0 ? sRows[r] : sRows[0]);
         else xr = (uint32_t)min(m0 + r, M - 1);
         const uint32_t wr = (uint32_t)min(n0 + r, N - 1);
-        xoff[i] = (xr * (uint32_t)K + 8u * ch) * 2u;
-        woff[i] = (wr * (uint32_t)K + 8u * ch) * 2u;
-        soff[i] = (wr * (uint32_t)KW + (uint32_t)(ch >> 2)) * 4u;
+        xoff[i] = (xr * (uint32_t)K + 8u * ch) * 2u + (uint32_t)kb0 * (BK * 2);
+        woff[i] = (wr * (uint32_t)K + 8u * ch) * 2u + (uint32_t)kb0 * (BK * 2);
+        soff[i] = (wr * (uint32_t)KW + (uint32_t)(ch >> 2)) * 4u + (uint32_t)kb0 * 8u;
     }
     const int sbit = (ch & 3) * 8;
     const int st_lane = 8 * wv * BK + 8 * lane;      // bf16 offset of the lane's slot, row block 0
@@ -666,6 +726,32 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     }
     if (t < KT) body(std::integral_constant<int, 0>{}, t);
 
+    // ---- a chunk of a split tile: store the partial sums (and, chunk 0, the
+    //      tile's row map and column origin); prefill_reduce_kernel, launched
+    //      next on the stream, adds the chunks in chunk order and writes y ----
+    if constexpr (GROUPED) {
+        const int nchunks = sInfo[7];
+        if (nchunks > 1) {
+            const int tid = threadIdx.x;
+            const int unit = sInfo[6];                   // leftover * nchunks + chunk
+            f32x4* mine = reinterpret_cast<f32x4*>(part) + (size_t)unit * kSplitVecs * kThreads;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        mine[((i * 4 + j) * 4 + q) * kThreads + tid] =
+                            f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            if (unit % nchunks == 0) {
+                int* meta = counters + 4 + kSplitMetaInts * (unit / nchunks);  // [rows 256][n0]
+                meta[tid] = sRows[tid];
+                if (tid == 0) meta[BM] = n0;
+            }
+            return;
+        }
+    }
+
     // ---- epilogue.  The W fragment is the MFMA's first operand, so acc[i][j][r]
     //      holds y[mrow + 32i][ncol + 32j + 8(r >> 2) + (r & 3)]: four
     //      consecutive columns per register quad ----
@@ -746,6 +832,50 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     }
 }
 
+// The chunks of the split leftover tiles: sum them in chunk order and write
+// the tiles' rows.  Sixteen blocks per leftover tile, each taking four of the
+// 64 partial vectors of every thread of the chunk blocks (the same thread
+// layout, so row and column follow as in the main epilogue).  Partials of
+// tile rows that hold no output row are not read.
+template <int ET>
+__global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(const float* __restrict__ part,
+                                                                  const int* __restrict__ split, void* __restrict__ y,
+                                                                  int N, int y_dtype) {
+    constexpr int kPerBlock = 4, kBlocks = kSplitVecs / kPerBlock;
+    const int nleft = split[0], S = split[1];
+    const int l = blockIdx.x / kBlocks, vb = blockIdx.x % kBlocks;
+    if (l >= nleft || S < 2) return;
+    const int* meta = split + 4 + kSplitMetaInts * l;
+    const int n0 = meta[BM];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int wm = wv >> 1, wn = wv & 1;
+    const f32x4* all = reinterpret_cast<const f32x4*>(part) + (size_t)l * S * kSplitVecs * kThreads;
+#pragma unroll
+    for (int vv = 0; vv < kPerBlock; ++vv) {
+        const int v = vb * kPerBlock + vv;              // (i * 4 + j) * 4 + q
+        const int i = v >> 4, j = (v >> 2) & 3, q = v & 3;
+        const int row = meta[wm * 128 + 32 * i + (lane & 31)];
+        if (row < 0) continue;
+        f32x4 pc[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            if (c < S) pc[c] = all[((size_t)c * kSplitVecs + v) * kThreads + tid];
+        f32x4 sum = pc[0];
+#pragma unroll
+        for (int c = 1; c < 8; ++c)
+            if (c < S) {
+                sum[0] += pc[c][0];
+                sum[1] += pc[c][1];
+                sum[2] += pc[c][2];
+                sum[3] += pc[c][3];
+            }
+        const int col = n0 + wn * 128 + 32 * j + 8 * q + 4 * (lane >> 5);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (col + e < N) store_y<ET>(y, (size_t)row * N + col + e, sum[e], y_dtype);
+    }
+}
+
 }  // namespace
 
 // The streaming kernel addresses x and W through buffer resources whose byte
@@ -761,20 +891,21 @@ template <int ET, bool GROUPED>
 void launch_stream_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                       const uint32_t* packed, const float* alpha, const int32_t* ids, int T,
                       void* y, int y_dtype, int tiles_m, int grid, int tiles_n,
-                      hipStream_t stream) {
+                      hipStream_t stream, float* part = nullptr, int* counters = nullptr, int room = 0,
+                      int g_tiles = 0) {
     const dim3 g(grid), block(kThreads);
     if (y_dtype != kF32 && N % 8 == 0)
         prefill_stream_kernel<ET, ET, true, GROUPED><<<g, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n, part, counters, room, g_tiles);
     else if (y_dtype != kF32)
         prefill_stream_kernel<ET, ET, false, GROUPED><<<g, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n, part, counters, room, g_tiles);
     else if (N % 4 == 0)
         prefill_stream_kernel<ET, kF32, true, GROUPED><<<g, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n, part, counters, room, g_tiles);
     else
         prefill_stream_kernel<ET, kF32, false, GROUPED><<<g, block, 0, stream>>>(
-            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n);
+            x, M, K, w, N, packed, alpha, ids, T, y, tiles_m, tiles_n, part, counters, room, g_tiles);
 }
 
 }  // namespace
@@ -806,22 +937,48 @@ bool prefill_grouped_supported(int M, int N, int K, int T) {
     return prefill_stream_supported(M, N, K) && T >= 1 && T <= kMaxGroupedTenants;
 }
 
+constexpr size_t kSplitMetaBytes = (4 + (size_t)kCUs * kSplitMetaInts) * sizeof(int);
+size_t prefill_split_bytes() { return (size_t)kCUs * kSplitChunkBytes + kSplitMetaBytes; }
+
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,
                                   const int32_t* tenant_ids, int T, void* y, int y_dtype,
-                                  int et, hipStream_t stream) {
+                                  int et, hipStream_t stream, void* scratch, size_t scratch_bytes) {
     // sum_t ceil(c_t / BM) over the U <= min(T, M) tenants present, with
     // sum_t c_t <= M, is at most (M + (BM - 1) * U) / BM
     const int64_t U = T < M ? T : M;
     const int tiles_m = (int)(((int64_t)M + (BM - 1) * U) / BM);
     const int tiles_n = (N + BN - 1) / BN;
-    const int grid = (tiles_m + 1) * tiles_n;
+    // partial-sum room: the split record sits at the start of the buffer,
+    // the chunks after it
+    int room = 0;
+    float* part = nullptr;
+    int* split = nullptr;
+    if (scratch != nullptr && scratch_bytes >= kSplitMetaBytes + 2 * kSplitChunkBytes) {
+        const size_t chunks = (scratch_bytes - kSplitMetaBytes) / kSplitChunkBytes;
+        room = (int)(chunks < (size_t)kCUs ? chunks : (size_t)kCUs);
+        split = static_cast<int*>(scratch);
+        part = reinterpret_cast<float*>(static_cast<char*>(scratch) + kSplitMetaBytes);
+    }
+    // blocks: every whole tile, and kCUs + room for the split chunks
+    int g_tiles = tiles_m * tiles_n;
+    if (g_tiles <= kCUs) room = 0;                     // one round at most: nothing to split
+    if (room > 0 && g_tiles < kCUs + room) g_tiles = kCUs + room;
+    const int grid = g_tiles + tiles_n;
     if (et == kF16)
         launch_stream_et<kF16, true>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype,
-                                     tiles_m, grid, tiles_n, stream);
+                                     tiles_m, grid, tiles_n, stream, part, split, room, g_tiles);
     else
         launch_stream_et<kBF16, true>(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype,
-                                      tiles_m, grid, tiles_n, stream);
+                                      tiles_m, grid, tiles_n, stream, part, split, room, g_tiles);
+    if (room > 0) {
+        // at most room / 2 leftover tiles are split (two chunks or more each)
+        const int rgrid = (kSplitVecs / 4) * (room / 2);
+        if (et == kF16)
+            prefill_reduce_kernel<kF16><<<rgrid, kThreads, 0, stream>>>(part, split, y, N, y_dtype);
+        else
+            prefill_reduce_kernel<kBF16><<<rgrid, kThreads, 0, stream>>>(part, split, y, N, y_dtype);
+    }
     return hipGetLastError();
 }
 

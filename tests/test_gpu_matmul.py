@@ -470,6 +470,58 @@ def test_grouped_prefill_effective_weight_exact(T):
     assert np.array_equal(y, ref)
 
 
+def _prompt_problem(M, N, K, T, yd, seed, prompts, dtype="bf16"):
+    p = wl.make_problem(M, N, K, T, seed=seed, multi_tenant=True, y_dtype=yd, dtype=dtype)
+    p.tenant_ids = wl.prompt_tenant_ids(np.random.default_rng(seed + 1), M, T, prompts)
+    tiles = sum(-(-int(c) // 256) for c in np.bincount(p.tenant_ids)) * -(-N // 256)
+    return p, tiles
+
+
+# More output tiles than CUs: the first 256 tiles run whole, the leftover ones
+# are split along K over the otherwise idle CUs and a second launch adds the
+# chunks' partial sums in chunk order.
+@pytest.mark.parametrize("M,N,K,T,yd", [(16640, 1024, 256, 5, "bf16"), (16640, 1024, 256, 5, "f32"),
+                                        (8320, 2048, 512, 3, "bf16"), (4096, 4096, 1024, 8, "bf16")])
+def test_grouped_prefill_split_tiles(M, N, K, T, yd):
+    p, tiles = _prompt_problem(M, N, K, T, yd, seed=M + N + K, prompts=12)
+    assert tiles > 256, tiles
+    log(f"grouped prefill with split tiles M={M} N={N} K={K} T={T} {yd} tiles={tiles}")
+    t = torch()
+    y1 = run_matmul(p, path=PREFILL)
+    y2 = run_matmul(p, path=PREFILL)
+    assert t.equal(y1.view(t.int16), y2.view(t.int16)), "split result differs between calls"
+    check(host_out(y1), oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+
+
+def test_grouped_prefill_split_fp16():
+    p, tiles = _prompt_problem(8320, 2048, 512, 3, "half", seed=77, prompts=10, dtype="f16")
+    assert tiles > 256, tiles
+    log(f"grouped prefill with split tiles, fp16, tiles={tiles}")
+    y = host_out(run_matmul(p, path=PREFILL))
+    ref = oracle.matmul(p.x, p.w, p.packed, p.alpha, p.tenant_ids, dtype="f16")
+    check(y, ref, p.x, p.w, p.alpha, p.tenant_ids, dtype="f16")
+
+
+def test_grouped_prefill_split_then_one_round():
+    # on one stream: a call that splits, then calls whose tile upper bound
+    # allows a split but whose actual tiles fit one round (the second launch
+    # must then leave y alone), then the split call again
+    p, tiles = _prompt_problem(4096, 4096, 512, 8, "bf16", seed=31, prompts=16)
+    assert tiles > 256, tiles
+    q = wl.make_problem(4096, 4096, 512, 200, seed=32, multi_tenant=True, y_dtype="bf16")
+    q.tenant_ids = np.repeat(np.array([7, 150], np.int32), 2048)    # 16 row tiles: one round
+    log(f"grouped prefill: split ({tiles} tiles), one round (256 tiles), split again")
+    t = torch()
+    a1 = run_matmul(p, path=PREFILL)
+    b = run_matmul(q, path=PREFILL)
+    a2 = run_matmul(p, path=PREFILL)
+    assert t.equal(a1.view(t.int16), a2.view(t.int16))
+    check(host_out(a1), oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+    rows = np.concatenate([np.arange(0, 4096, 61), [2047, 2048, 4095]])
+    check(host_out(b[t.from_numpy(rows).cuda()]), oracle_y(q, rows=rows), q.x, q.w, q.alpha,
+          q.tenant_ids[rows], rows=rows)
+
+
 def test_grouped_prefill_tenant_limit():
     import paper_2609_36800_amd as bd
     M, N, K = 300, 64, 128
