@@ -14,8 +14,9 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - All array arguments are DEVICE pointers owned by the caller; the library
- *    never allocates, frees or retains them, keeps no global state, and is
- *    re-entrant.  Arrays are dense and row-major.
+ *    never frees or retains them.  Arrays are dense and row-major.  The only
+ *    memory the library allocates is the grouped prefill's workspace (see
+ *    bitdelta_matmul_noalloc); calls on different streams are independent.
  *  - Work is enqueued asynchronously on `stream` (0 = the null stream); the
  *    functions return once the kernels are launched.
  *  - Arguments are checked on the host before anything is launched; a
@@ -179,6 +180,34 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K,
                           const uint32_t* packed_s, const float* alpha,
                           const int32_t* tenant_ids, int32_t T, int in_dtype,
                           void* y, int y_dtype, int path, hipStream_t stream);
+
+/*
+ * Allocation-free form of bitdelta_matmul_typed, for callers that cannot
+ * allocate device memory: code under graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Arguments, results and errors are those
+ * of bitdelta_matmul_typed; the outputs are bitwise identical to its.
+ *
+ * bitdelta_matmul_typed may allocate, once per (device, stream), the grouped
+ * prefill's partial-sum workspace (the fp32 partial sums of output tiles split
+ * along K when there are more tiles than compute units).  This form never
+ * calls hipMalloc or any allocating routine: it uses a fixed array of
+ * 67,375,120 bytes in the library's device memory (64 MiB of partial sums and
+ * 266,256 bytes of split record), which each GPU the library runs on holds
+ * until the process ends.  That size covers the largest split, so no request
+ * is refused for its size; the only limits are bitdelta_matmul_typed's.  On
+ * its first call on a device the address of that device's array is looked up
+ * (hipGetSymbolAddress); BITDELTA_ERR_HIP if the runtime cannot give it.
+ *
+ * All calls of this form on one GPU share the array: calls that overlap in
+ * time on one GPU (different streams, or different host threads) race and
+ * may produce wrong results.  Calls in order on one stream are safe.  The
+ * array keeps the last call's contents; every call writes what it reads.
+ */
+int bitdelta_matmul_noalloc(const uint16_t* x, int64_t M, int64_t K,
+                            const uint16_t* w_base, int64_t N,
+                            const uint32_t* packed_s, const float* alpha,
+                            const int32_t* tenant_ids, int32_t T, int in_dtype,
+                            void* y, int y_dtype, int path, hipStream_t stream);
 
 /* The path bitdelta_matmul picks for these sizes (no side effects). */
 int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_tenant_ids);

@@ -32,6 +32,7 @@ EXPORTED = (
     "bitdelta_matmul",
     "bitdelta_matmul_with_path",
     "bitdelta_matmul_typed",
+    "bitdelta_matmul_noalloc",
     "bitdelta_matmul_path",
     "bitdelta_status_string",
     "bitdelta_version",
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH):
     lib.bitdelta_matmul_with_path.restype = I
     lib.bitdelta_matmul_typed.argtypes = [P, I64, I64, P, I64, P, P, P, I32, I, P, I, I, P]
     lib.bitdelta_matmul_typed.restype = I
+    lib.bitdelta_matmul_noalloc.argtypes = [P, I64, I64, P, I64, P, P, P, I32, I, P, I, I, P]
+    lib.bitdelta_matmul_noalloc.restype = I
     lib.bitdelta_matmul_path.argtypes = [I64, I64, I64, I32, I]
     lib.bitdelta_matmul_path.restype = I
     lib.bitdelta_status_string.argtypes = [I]

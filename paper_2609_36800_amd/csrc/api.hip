@@ -11,6 +11,10 @@
 #include "../../include/bitdelta.h"
 #include "internal.h"
 
+// The allocation-free entry point's scratch (see device_scratch below).
+constexpr size_t kScratchBytes = bitdelta::kPrefillSplitBytes;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
 namespace {
 
 constexpr int kSkinnyRows = 64;
@@ -123,6 +127,33 @@ void* stream_workspace(hipStream_t stream, size_t bytes) {
     return p;
 }
 
+// Scratch of the allocation-free entry point: one fixed device array, each
+// GPU holding its own copy for the life of the process.  Host code reaches it
+// only through the address hipGetSymbolAddress gives for the current device
+// (the array's name is not a device address on the host); that address is
+// taken once per device, on the device's first allocation-free call.  Its
+// size is the grouped prefill's full split, so the allocation-free calls split
+// exactly as bitdelta_matmul does.  Every call writes what it reads there:
+// nothing has to start at zero.  Calls that overlap on one GPU share it and
+// race.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch`, or null if the runtime cannot
+// give it.
+void* device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
 // More output tiles than CUs is possible (the grouped GEMM may split).
 bool grouped_may_split(int64_t M, int64_t N, int32_t T) {
     const int64_t U = T < M ? T : M;
@@ -218,10 +249,16 @@ int bitdelta_matmul_path(int64_t M, int64_t N, int64_t K, int32_t T, int has_ten
     return choose_path(M, N, K, T, has_tenant_ids);
 }
 
-int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
-                          int64_t N, const uint32_t* packed_s, const float* alpha,
-                          const int32_t* tenant_ids, int32_t T, int in_dtype, void* y,
-                          int y_dtype, int path, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The matmul behind every entry point.  noalloc: the grouped prefill's
+// partial sums go to the static scratch array instead of the per-stream
+// workspace, and nothing is allocated.
+int matmul_impl(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base, int64_t N,
+                const uint32_t* packed_s, const float* alpha, const int32_t* tenant_ids, int32_t T,
+                int in_dtype, void* y, int y_dtype, int path, hipStream_t stream, bool noalloc) {
     int rc = check_matmul(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, in_dtype, y, y_dtype);
     if (rc != BITDELTA_OK) return rc;
     if (path == BITDELTA_PATH_AUTO) path = choose_path(M, N, K, T, tenant_ids != nullptr);
@@ -241,9 +278,15 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_
         void* ws = nullptr;
         size_t ws_bytes = 0;
         if (grouped_may_split(M, N, T)) {
-            ws_bytes = bitdelta::prefill_split_bytes();
-            ws = stream_workspace(stream, ws_bytes);
-            (void)hipGetLastError();      // a failed allocation only disables the split
+            if (noalloc) {
+                ws = device_scratch();
+                if (ws == nullptr) return BITDELTA_ERR_HIP;
+                ws_bytes = kScratchBytes;
+            } else {
+                ws_bytes = bitdelta::prefill_split_bytes();
+                ws = stream_workspace(stream, ws_bytes);
+                (void)hipGetLastError();  // a failed allocation only disables the split
+            }
         }
         return hip_status(bitdelta::launch_prefill_grouped(x, (int)M, (int)K, w_base, (int)N,
                                                            packed_s, alpha, tenant_ids, (int)T, y,
@@ -264,6 +307,26 @@ int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_
         if (rc != BITDELTA_OK) return rc;
     }
     return BITDELTA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int bitdelta_matmul_typed(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
+                          int64_t N, const uint32_t* packed_s, const float* alpha,
+                          const int32_t* tenant_ids, int32_t T, int in_dtype, void* y,
+                          int y_dtype, int path, hipStream_t stream) {
+    return matmul_impl(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, in_dtype, y, y_dtype, path,
+                       stream, false);
+}
+
+int bitdelta_matmul_noalloc(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,
+                            int64_t N, const uint32_t* packed_s, const float* alpha,
+                            const int32_t* tenant_ids, int32_t T, int in_dtype, void* y,
+                            int y_dtype, int path, hipStream_t stream) {
+    return matmul_impl(x, M, K, w_base, N, packed_s, alpha, tenant_ids, T, in_dtype, y, y_dtype, path,
+                       stream, true);
 }
 
 int bitdelta_matmul_with_path(const uint16_t* x, int64_t M, int64_t K, const uint16_t* w_base,

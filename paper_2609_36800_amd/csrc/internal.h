@@ -68,6 +68,9 @@ hipError_t launch_prefill(const uint16_t* x, int M, int K, const uint16_t* w, in
 // can hold their fp32 partial sums and per-tile counters; the counters must be
 // zero on entry and are left zero.  scratch may be null (no split).
 size_t prefill_split_bytes();
+// prefill_split_bytes() as a constant: 256 chunks of 256 x 256 fp32 partial
+// sums and the split record (4 ints, then 260 per leftover tile)
+constexpr size_t kPrefillSplitBytes = (size_t)256 * 256 * 256 * 4 + (4 + (size_t)256 * (256 + 4)) * 4;
 bool prefill_grouped_supported(int M, int N, int K, int T);
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,

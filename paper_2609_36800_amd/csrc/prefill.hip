@@ -938,7 +938,8 @@ bool prefill_grouped_supported(int M, int N, int K, int T) {
 }
 
 constexpr size_t kSplitMetaBytes = (4 + (size_t)kCUs * kSplitMetaInts) * sizeof(int);
-size_t prefill_split_bytes() { return (size_t)kCUs * kSplitChunkBytes + kSplitMetaBytes; }
+static_assert((size_t)kCUs * kSplitChunkBytes + kSplitMetaBytes == kPrefillSplitBytes, "split buffer size");
+size_t prefill_split_bytes() { return kPrefillSplitBytes; }
 
 hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_t* w, int N,
                                   const uint32_t* packed, const float* alpha,
