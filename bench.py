@@ -301,7 +301,8 @@ def context_ceilings(dev, warmup):
     library's): torch's elementwise negation kernel (one buffer read, another
     written), as a bandwidth ceiling for a large transfer and for one transfer of
     the decode launch's size (36 MB read + 36 MB written, buffers rotating over
-    more than twice the Infinity Cache), and torch.matmul's
+    more than twice the Infinity Cache), torch's sum reading 36 MB per launch
+    (a read-only ceiling at the decode launch's size), and torch.matmul's
     plain bf16 GEMM at 4096^3 (no decode), the matrix-core reference for the fused
     prefill.  Context only: none of them is a figure of this library."""
     import torch
@@ -327,7 +328,14 @@ def context_ceilings(dev, warmup):
     secs, graphed = time_calls(calls, 1)
     out["elementwise_copy_36MB"] = {"us": secs * 1e6, "GBps": 2 * n36 * 2 / secs / 1e9, "bytes": 2 * n36 * 2,
                         "graphed": graphed, "buffer_sets": len(sets)}
-    del sets, calls
+    # read-only: a sum over the same 36 MB (the decode launch reads, and
+    # writes next to nothing)
+    sums = torch.empty(len(sets), dtype=torch.float32, device=dev)
+    calls = [(lambda i=i, s=s: torch.sum(s[0], dtype=torch.float32, out=sums[i])) for i, s in enumerate(sets)] * 4
+    secs, graphed = time_calls(calls, 1)
+    out["read_sum_36MB"] = {"us": secs * 1e6, "GBps": n36 * 2 / secs / 1e9, "bytes": n36 * 2,
+                            "graphed": graphed, "buffer_sets": len(sets)}
+    del sets, calls, sums
     g = torch.Generator(device=dev)
     g.manual_seed(5)
     x = torch.randn((4096, 4096), generator=g, device=dev).to(torch.bfloat16)
@@ -693,6 +701,10 @@ def main():
         roofline["same_run_copy_ceiling"] = {
             "GBps": cop, "what": "torch elementwise copy, 36 MB read + 36 MB written per launch, "
                                  "16 rotating buffer pairs", "frac_of_ceiling": achieved / cop}
+        rd = context["read_sum_36MB"]["GBps"]
+        roofline["same_run_read_ceiling"] = {
+            "GBps": rd, "what": "torch sum reading 36 MB per launch (one launch's read of the decode "
+                                "pair's size), 16 rotating buffers", "frac_of_ceiling": achieved / rd}
     else:
         context = {}
     context["paper"] = PAPER_CONTEXT
