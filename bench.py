@@ -248,6 +248,26 @@ def llama_sweep(dev, launcher, warmup):
             "per_matrix": per_matrix}
 
 
+def decode_size_sweep(dev, launcher, warmup):
+    """The streaming decode kernel (M = 1, K = 4096) at four launch sizes,
+    N = 4096 .. 32768 (36 .. 290 MB of W and signs per launch), each on buffer
+    sets rotating over more than twice the Infinity Cache.  A least-squares line
+    time = fixed + bytes / rate separates the per-launch ramp and drain from the
+    streaming rate, which is what bounds one 36 MB launch."""
+    pts = []
+    for N in (4096, 8192, 16384, 32768):
+        r = bench_workload(f"decode M=1, N={N}", [(1, N, 4096)], 1, False,
+                           lambda M, N_, K: 2 * M * N_ * K, 40, warmup, dev, launcher, seed=700 + N)
+        pts.append({"N": N, "bytes": r["bytes_per_step"], "us": r["avg_launch_us"], "TBps": r["TBps"]})
+    xs = [p["bytes"] for p in pts]
+    ys = [p["us"] for p in pts]
+    mx, my = sum(xs) / len(xs), sum(ys) / len(ys)
+    slope = sum((a - mx) * (b - my) for a, b in zip(xs, ys)) / sum((a - mx) ** 2 for a in xs)
+    fixed = my - slope * mx
+    return {"workload": "decode launch-size sweep: x 1x4096, W_base N x 4096, N = 4096 .. 32768",
+            "points": pts, "fit": {"fixed_us": fixed, "asymptotic_GBps": 1e-3 / slope}}
+
+
 def bench_compress(dev, lib, steps, warmup):
     """Delta compression of LLaMA-7B-gate-shaped weights (11008x4096 bf16 fine and
     base -> packed signs, per-row |delta| sums, scale), buffer sets rotating over
@@ -328,14 +348,7 @@ def context_ceilings(dev, warmup):
     secs, graphed = time_calls(calls, 1)
     out["elementwise_copy_36MB"] = {"us": secs * 1e6, "GBps": 2 * n36 * 2 / secs / 1e9, "bytes": 2 * n36 * 2,
                         "graphed": graphed, "buffer_sets": len(sets)}
-    # read-only: a sum over the same 36 MB (the decode launch reads, and
-    # writes next to nothing)
-    sums = torch.empty(len(sets), dtype=torch.float32, device=dev)
-    calls = [(lambda i=i, s=s: torch.sum(s[0], dtype=torch.float32, out=sums[i])) for i, s in enumerate(sets)] * 4
-    secs, graphed = time_calls(calls, 1)
-    out["read_sum_36MB"] = {"us": secs * 1e6, "GBps": n36 * 2 / secs / 1e9, "bytes": n36 * 2,
-                            "graphed": graphed, "buffer_sets": len(sets)}
-    del sets, calls, sums
+    del sets, calls
     g = torch.Generator(device=dev)
     g.manual_seed(5)
     x = torch.randn((4096, 4096), generator=g, device=dev).to(torch.bfloat16)
@@ -694,6 +707,8 @@ def main():
         workloads.append(pf16)
         workloads.append(llama_sweep(dev, launcher, args.warmup))
         workloads.append(bench_compress(dev, launcher.lib, 50, args.warmup))
+        sweep = decode_size_sweep(dev, launcher, args.warmup)
+        workloads.append(sweep)
         context = context_ceilings(dev, args.warmup)
         # the same-run read ceiling for one launch of the headline's size: a
         # library copy moving the decode launch's W + signs in and the same out
@@ -701,10 +716,12 @@ def main():
         roofline["same_run_copy_ceiling"] = {
             "GBps": cop, "what": "torch elementwise copy, 36 MB read + 36 MB written per launch, "
                                  "16 rotating buffer pairs", "frac_of_ceiling": achieved / cop}
-        rd = context["read_sum_36MB"]["GBps"]
-        roofline["same_run_read_ceiling"] = {
-            "GBps": rd, "what": "torch sum reading 36 MB per launch (one launch's read of the decode "
-                                "pair's size), 16 rotating buffers", "frac_of_ceiling": achieved / rd}
+        fit = sweep["fit"]
+        roofline["launch_size_fit"] = {
+            "what": "the same decode kernel (M=1, K=4096) timed at N = 4096 .. 32768 (36 .. 290 MB per "
+                    "launch); least-squares time = fixed_us + bytes / asymptotic rate",
+            "fixed_us": fit["fixed_us"], "asymptotic_GBps": fit["asymptotic_GBps"],
+            "frac_of_asymptote_at_headline_size": achieved / fit["asymptotic_GBps"]}
     else:
         context = {}
     context["paper"] = PAPER_CONTEXT
