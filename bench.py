@@ -494,16 +494,19 @@ def pmc_pass(steps, workload="decode"):
     multi: `steps` launches of the batched kernel at 64 rows, 8 tenants,
     4096x4096, on 12 rotating buffer sets.  mtdecode: `steps` launches of the
     multi-tenant decode workload (32 rows, 16 tenants, 11008x4096) on 4
-    rotating buffer sets, with the distinct tenants of each set printed."""
+    rotating buffer sets, with the distinct tenants of each set printed.  gate:
+    the same at the LLaMA-shaped sweep's gate / up shape (64 rows, 8 tenants,
+    11008x4096)."""
     import torch
     import paper_2609_36800_amd as bd
     dev = torch.device("cuda:0")
     launcher = Launcher(bd.load_library())
-    if workload == "mtdecode":
+    if workload in ("mtdecode", "gate"):
+        M, T = (32, 16) if workload == "mtdecode" else (64, 8)
         calls, keep, distinct = [], [], []
         for r in range(4):
-            d = make_sets(1, 32, 11008, 4096, 16, True, 21 + r, dev)[0]
-            y = torch.empty((32, 11008), dtype=torch.bfloat16, device=dev)
+            d = make_sets(1, M, 11008, 4096, T, True, 21 + r, dev)[0]
+            y = torch.empty((M, 11008), dtype=torch.bfloat16, device=dev)
             keep.append((d, y))
             distinct.append(int(torch.unique(d["tenant_ids"]).numel()))
             calls.append(launcher.matmul(d["x"], d["w"], d["packed"], d["alpha"],
@@ -618,7 +621,7 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=10.0)
     ap.add_argument("--pmc-pass", action="store_true",
                     help="only launch the headline kernels and a calibration copy (for rocprofv3 --pmc)")
-    ap.add_argument("--pmc-workload", choices=("decode", "prefill", "multi", "mtdecode"), default="decode",
+    ap.add_argument("--pmc-workload", choices=("decode", "prefill", "multi", "mtdecode", "gate"), default="decode",
                     help="what --pmc-pass launches")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write the HBM traffic record from two --pmc runs of --pmc-pass (no GPU needed)")
