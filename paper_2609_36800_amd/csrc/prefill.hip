@@ -281,23 +281,52 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
     }
     __syncthreads();
 
-    // tiles per tenant; exclusive scan over tenants (thread i takes a run of them)
+    // Row tiles, in this order: every tenant's full (256-row) tiles, tenant by
+    // tenant; then the tenants' last, partly filled tiles, in eight classes of
+    // decreasing row count (224-255 rows, 192-223, ..., 1-31), tenant by tenant
+    // within a class.  So the row tiles at the end -- the ones split when there
+    // are more tiles than CUs -- hold the fewest rows, and their partial sums
+    // (stored only for rows that exist) the fewest bytes.  Class 0 counts full
+    // tiles, class 1 + j partial tiles of row class j; one exclusive scan per
+    // class over the tenants (thread i takes a run of tenants).
+    constexpr int kClasses = 9;
     const int per = (T + kThreads - 1) / kThreads;
     const int t_beg = min(T, tid * per), t_end = min(T, t_beg + per);
     auto count = [&](int t) { return hist[t] + hist[T + t] + hist[2 * T + t] + hist[3 * T + t]; };
-    int s = 0;
-    for (int t = t_beg; t < t_end; ++t) s += (count(t) + BM - 1) / BM;
-    int incl = s;
+    auto class_of_last = [](int c) { return 1 + (BM - 1 - c % BM) / 32; };   // c % BM != 0
+    int sc[kClasses], ex[kClasses];
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-        const int o = __shfl_up(incl, d);
-        if (lane >= d) incl += o;
+    for (int k = 0; k < kClasses; ++k) sc[k] = 0;
+    for (int t = t_beg; t < t_end; ++t) {
+        const int c = count(t);
+        sc[0] += c / BM;
+        if (c % BM != 0) {
+            const int k = class_of_last(c);
+#pragma unroll
+            for (int kk = 1; kk < kClasses; ++kk) sc[kk] += kk == k;
+        }
     }
-    if (lane == 63) info[wv] = incl;
+#pragma unroll
+    for (int k = 0; k < kClasses; ++k) {
+        int inc = sc[k];
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int o = __shfl_up(inc, d);
+            if (lane >= d) inc += o;
+        }
+        if (lane == 63) rows[4 * k + wv] = inc;
+        ex[k] = inc - sc[k];
+    }
     __syncthreads();
-    const int total = info[0] + info[1] + info[2] + info[3];
-    int excl = incl - s;
-    for (int w2 = 0; w2 < wv; ++w2) excl += info[w2];
+    int cls_first[kClasses + 1];                 // first row tile of each class
+    cls_first[0] = 0;
+#pragma unroll
+    for (int k = 0; k < kClasses; ++k) {
+        cls_first[k + 1] = cls_first[k] + rows[4 * k] + rows[4 * k + 1] + rows[4 * k + 2] + rows[4 * k + 3];
+        for (int w2 = 0; w2 < wv; ++w2) ex[k] += rows[4 * k + w2];
+    }
+    const int total = cls_first[kClasses];
+    __syncthreads();            // the totals are read before info[4..5] and rows[] are reused
     const int ntiles = total * tiles_n;
     const int S = split_chunks(ntiles, room, KT);
     // block 0 records this call's split for the reduction launch that follows
@@ -318,17 +347,50 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
     }
     if (tile_idx >= ntiles) return false;
     int tile_v;
-    tile_of(tile_idx, total, tiles_n, tile_v, tile_n);
-    if (tile_v >= excl && tile_v < excl + s) {
-        int first = excl;
+    if (S > 1 && kCUs % tiles_n == 0) {
+        // the whole tiles are the first kCUs / tiles_n row tiles (grouped for
+        // L2 as in the one-round case); the leftover ones follow row by row
+        if (tile_idx < kCUs) {
+            tile_of(tile_idx, kCUs / tiles_n, tiles_n, tile_v, tile_n);
+        } else {
+            const int l = tile_idx - kCUs;
+            tile_v = kCUs / tiles_n + l / tiles_n;
+            tile_n = l % tiles_n;
+        }
+    } else {
+        tile_of(tile_idx, total, tiles_n, tile_v, tile_n);
+    }
+    int k = 0;
+#pragma unroll
+    for (int kk = 1; kk < kClasses; ++kk) k += tile_v >= cls_first[kk];
+    const int pv = tile_v - cls_first[k];        // index within its class
+    int exk = 0, sck = 0;
+#pragma unroll
+    for (int kk = 0; kk < kClasses; ++kk)
+        if (kk == k) {
+            exk = ex[kk];
+            sck = sc[kk];
+        }
+    if (pv >= exk && pv < exk + sck) {
+        int first = exk;
         for (int t = t_beg; t < t_end; ++t) {
-            const int nt = (count(t) + BM - 1) / BM;
-            if (tile_v < first + nt) {
-                info[4] = t;
-                info[5] = tile_v - first;
-                break;
+            const int c = count(t);
+            if (k == 0) {
+                const int nf = c / BM;
+                if (pv < first + nf) {
+                    info[4] = t;
+                    info[5] = pv - first;
+                    break;
+                }
+                first += nf;
+            } else if (c % BM != 0 && class_of_last(c) == k) {
+                if (pv == first) {
+                    info[4] = t;
+                    info[5] = c / BM;
+                    break;
+                }
+                ++first;
             }
-            first += nt;
         }
     }
     rows[tid] = -1;
@@ -735,14 +797,18 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
             const int tid = threadIdx.x;
             const int unit = sInfo[6];                   // leftover * nchunks + chunk
             f32x4* mine = reinterpret_cast<f32x4*>(part) + (size_t)unit * kSplitVecs * kThreads;
+            // partials of tile rows that hold no output row are neither stored
+            // nor read by the reduction
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) {
+                if (sRows[wm * 128 + 32 * i + (lane & 31)] < 0) continue;
 #pragma unroll
                 for (int j = 0; j < 4; ++j)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
                         mine[((i * 4 + j) * 4 + q) * kThreads + tid] =
                             f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+            }
             if (unit % nchunks == 0) {
                 int* meta = counters + 4 + kSplitMetaInts * (unit / nchunks);  // [rows 256][n0]
                 meta[tid] = sRows[tid];
