@@ -14,18 +14,20 @@
 // workgroup (4 waves, 2x2) owns a 256x256 output tile, each wave 128x128 =
 // 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 fp32 accumulators per lane).  Per
 // 64-wide k-tile:
-//   * the x tile is loaded into registers one tile ahead by buffer loads
-//     (32-bit per-lane offsets, the k offset in a scalar register) and
-//     written to one of two LDS buffers;
+//   * the x tile goes global -> LDS by direct copies (no registers), into
+//     one of two LDS buffers as soon as the barrier frees it, a tile ahead
+//     of its use; one explicit vmcnt wait before the next barrier covers
+//     them (measured 4% faster in bf16 than staging x through registers);
 //   * the raw W tile and its sign words are loaded into registers two tiles
-//     ahead (two register sets), and the effective weights of the next tile
-//     are formed and written to the other of two LDS buffers while the
+//     ahead (buffer loads: 32-bit per-lane offsets, the k offset in a scalar
+//     register; two register sets), and the effective weights of the next
+//     tile are formed and written to the other of two LDS buffers while the
 //     matrix cores work on the current one: the 64 MFMAs of a k-tile are
 //     issued one per scheduling slot, and each slot carries a share of the
 //     decode (one bf16 pair), the LDS writes and the next loads;
 //   * one barrier per k-tile publishes both buffers.
 // The two LDS buffers of each operand are separate objects so the compiler
-// can tell a copy into one from a read of the other and count the copies
+// can tell a write into one from a read of the other and count the writes
 // exactly when it places its waits.
 // Every W element is decoded once per workgroup; with alpha's sign moved onto
 // W (s*W + alpha, rounded, then the sign restored -- round-to-nearest-even is
@@ -625,8 +627,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     // wave-uniform k-tile offset in an SGPR, so no address arithmetic is
     // spent per load.  Row indices are clamped, so every access is in range.
     constexpr int kRawBufferFlags = 0x00020000;  // untyped 32-bit data format
-    const __amdgpu_buffer_rsrc_t xres = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<uint16_t*>(x), (short)0, (int)((uint32_t)M * (uint32_t)K * 2u), kRawBufferFlags);
     const __amdgpu_buffer_rsrc_t wres = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<uint16_t*>(w), (short)0, (int)((uint32_t)N * (uint32_t)K * 2u), kRawBufferFlags);
     const __amdgpu_buffer_rsrc_t sres = __builtin_amdgcn_make_buffer_rsrc(
@@ -638,12 +638,15 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     auto load_s = [&](uint32_t& dst, int i, int kt) {
         dst = __builtin_amdgcn_raw_buffer_load_b32(sres, (int)soff[i], kt * 8, 0);
     };
-    auto load_x = [&](u32x4& dst, int i, int kt) {
-        dst = __builtin_amdgcn_raw_buffer_load_b128(xres, (int)xoff[i], kt * (BK * 2), 0);
-    };
     auto sign_word = [&](uint32_t d) {
         const uint32_t byte = (d >> sbit) & 0xFFu;
         return opaque(byte | (byte << 15));
+    };
+    // x chunk i of k-tile kt straight into LDS by a global->LDS copy: lane l
+    // lands at slot l of the wave's 1 KB, the layout st_lane describes
+    auto copy_x = [&](uint16_t* buf, int i, int kt) {
+        copy16_to_lds(reinterpret_cast<const char*>(x) + xoff[i] + (size_t)kt * (BK * 2),
+                      buf + i * 32 * BK + 8 * wv * BK);
     };
     auto frag = [&](const uint16_t* buf, int row0, int blk, int kk) {
         return *reinterpret_cast<const u32x4*>(buf + row0 + blk * 32 * BK + rdo[kk]);
@@ -665,15 +668,17 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     uint32_t s0[8], s1[8];
 
     // ---- prologue: tile 0 and chunks 0..1 of tile 1 staged, registers primed ----
-    u32x4 xr[8];
     const int k1 = min(1, KT - 1), k2 = min(2, KT - 1), k3 = min(3, KT - 1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, 0); load_s(s0[i], i, 0); load_x(xr[i], i, 0); }
+    for (int i = 0; i < 8; ++i) copy_x(sA0, i, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) copy_x(sA1, i, k1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, 0); load_s(s0[i], i, 0); }
 #pragma unroll
     for (int i = 0; i < 8; ++i) { load_w(w1[i], i, k1); load_s(s1[i], i, k1); }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
-        *reinterpret_cast<u32x4*>(sA0 + i * 32 * BK + st_lane) = xr[i];
         const uint32_t sw0 = sign_word(s0[i]);
         u32x4 o;
 #pragma unroll
@@ -681,10 +686,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         *reinterpret_cast<u32x4*>(sB0 + i * 32 * BK + st_lane) = o;
     }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) { load_x(xr[i], i, k1); load_w(w0[i], i, k2); load_s(s0[i], i, k2); }
+    for (int i = 0; i < 8; ++i) { load_w(w0[i], i, k2); load_s(s0[i], i, k2); }
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-        *reinterpret_cast<u32x4*>(sA1 + i * 32 * BK + st_lane) = xr[i];
         const uint32_t sw1 = sign_word(s1[i]);
         u32x4 o;
 #pragma unroll
@@ -692,8 +696,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         *reinterpret_cast<u32x4*>(sB1 + i * 32 * BK + st_lane) = o;
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) { load_x(xr[i], i, k2); load_w(w1[i], i, k3); load_s(s1[i], i, k3); }
+    for (int i = 0; i < 2; ++i) { load_w(w1[i], i, k3); load_s(s1[i], i, k3); }
     uint32_t sw = sign_word(s1[2]);
+    wait_vm_lgkm0<0>();                              // x of tiles 0 and 1 in LDS
     raw_barrier();
     u32x4 fa[4], fb[4], na[4], nb[4];
     fa[0] = frag(sA0, a_row0, 0, 0);
@@ -701,6 +706,13 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
     for (int j = 0; j < 4; ++j) fb[j] = frag(sB0, b_row0, j, 0);
 #pragma unroll
     for (int i = 1; i < 4; ++i) fa[i] = frag(sA0, a_row0, i, 0);
+
+    // Loads per slot: each run of eight slots issues one sign-word load (its
+    // seventh slot) and one W load (its eighth).  The x copies of tile t+2 go
+    // out in slots 48..55 of body t, the last before slot 55's W load; up to
+    // the barrier of body t+1 (slot 48) come that W load, the two loads of
+    // slots 56..63 and the twelve of body t+1's slots 0..47.
+    constexpr int kXWait = 1 + 2 + 12;
 
     // Body t: the 64 MFMAs of tile t.  Fragments are always read one k-step
     // ahead, so the barrier that publishes tile t+1 sits between k-steps 2
@@ -722,7 +734,6 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         u32x4(&wn2)[8] = pick<P>(w0, w1);          // tile t+2
         uint32_t(&sn2)[8] = pick<P>(s0, s1);
         const int kr1 = min(t + 3, KT - 1), kr2 = min(t + 4, KT - 1);
-        const int kx1 = min(t + 2, KT - 1), kx2 = min(t + 3, KT - 1);
 
         PairWork pw;
         u32x4 o;
@@ -730,13 +741,18 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
             if (b == 3) {
-                // this wave's LDS writes of tile t+1 are complete; publish them
+                // this wave's LDS writes of tile t+1 are complete, and so are its
+                // x copies of tile t+1 (the previous body's slots 48..55): after
+                // them came kXWait loads (wait_vm_lgkm0 below); publish them
+                wait_vm_lgkm0<kXWait>();
                 raw_barrier();
                 __builtin_amdgcn_sched_barrier(0);
             }
 #pragma unroll
             for (int m = 0; m < 16; ++m) {
                 const int i = m >> 2, j = m & 3;
+                // tile t's buffers are free after the barrier: x of tile t+2
+                if (b == 3 && m < 8) copy_x(Ac, m, min(t + 2, KT - 1));
                 acc[i][j] = mfma32<ET>(fb[j], fa[i], acc[i][j]);
                 if (m < 8) {
                     const uint16_t* abuf = b < 3 ? Ac : An;
@@ -753,9 +769,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                 u32x4(&ws)[8] = first ? wn1 : wn2;
                 uint32_t(&ss)[8] = first ? sn1 : sn2;
                 uint16_t* const dst = first ? Bn : Bc;
-                uint16_t* const xdst = first ? An : Ac;
                 const int kr = first ? kr1 : kr2;
-                const int kx = first ? kx1 : kx2;
                 if constexpr (ET == kF16) {
                     if ((u & 1) == 0) o[u >> 1] = fuse_pair_f16(ws[c][u >> 1], sw, u >> 1, neg_alpha_h);
                 } else {
@@ -769,9 +783,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
                 }
                 if (u == 7) {
                     *reinterpret_cast<u32x4*>(dst + c * 32 * BK + st_lane) = o;
-                    *reinterpret_cast<u32x4*>(xdst + c * 32 * BK + st_lane) = xr[c];
                     load_w(ws[c], c, kr);
-                    load_x(xr[c], c, kx);
                     sw = sw_next;
                 }
                 __builtin_amdgcn_sched_barrier(0);
@@ -787,6 +799,7 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_stream_kernel(
         body(std::integral_constant<int, 1>{}, t + 1);
     }
     if (t < KT) body(std::integral_constant<int, 0>{}, t);
+    wait_vm_lgkm0<0>();                              // the last x copies are in before LDS is reused
 
     // ---- a chunk of a split tile: store the partial sums (and, chunk 0, the
     //      tile's row map and column origin); prefill_reduce_kernel, launched
