@@ -77,4 +77,12 @@ hipError_t launch_prefill_grouped(const uint16_t* x, int M, int K, const uint16_
                                   const int32_t* tenant_ids, int T, void* y, int y_dtype,
                                   int et, hipStream_t stream, void* scratch, size_t scratch_bytes);
 
+// Batched matmul, wide form (wide.hip): 17 to 64 rows, at most 16 distinct
+// tenants, K a multiple of 128, 48 or 64 features per workgroup, where those
+// feature groups fill the CUs (wide_supported).
+bool wide_supported(int M, int N, int K, int T);
+hipError_t launch_wide(const uint16_t* x, int M, int K, const uint16_t* w, int N, const uint32_t* packed,
+                       const float* alpha, const int32_t* tenant_ids, int T, void* y, int y_dtype, int et,
+                       hipStream_t stream);
+
 }  // namespace bitdelta

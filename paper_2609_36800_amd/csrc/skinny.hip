@@ -353,6 +353,8 @@ hipError_t launch_skinny_et(const uint16_t* x, int M, int K, const uint16_t* w, 
             default: return launch_single_mb<ET, 4>(x, M, K, w, N, packed, alpha, y, y_dtype, stream);
         }
     }
+    if (wide_supported(M, N, K, T))
+        return launch_wide(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, ET, stream);
     if (batched_supported(M, N, K, T))
         return launch_batched(x, M, K, w, N, packed, alpha, tenant_ids, T, y, y_dtype, ET, stream);
     if (multi_supported(K))
