@@ -30,7 +30,8 @@
 // super-tile j, early enough that the in-order wait for a tile also covers the
 // signs it reads.  Every wave issues the same number of copies per step (past
 // the end of K, or with no real work, a copy of one hot line instead), so one
-// s_waitcnt vmcnt count and one barrier per step hand a tile over.  The loop
+// s_waitcnt vmcnt count and one barrier per step hand a tile over.  Operands
+// are read from LDS one step ahead of the arithmetic that uses them.  The loop
 // runs sixteen steps per pass, so ring slots, super-tile phases and sign words
 // are compile-time offsets of the LDS reads.
 #include "device.h"
@@ -310,58 +311,81 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
 #pragma unroll
             for (int b = 0; b < FB; ++b) accs[i][b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-        // step t (I = t mod 16): ring slot I mod NB, sign buffer (I >> 3) & 1,
+        // the LDS operands of one tile: sign words, x fragments, and the natural
+        // x rows and W fragments of the base pairs
+        struct Ops {
+            uint2 s2[NA1][FB];
+            u32x4 xa[NA1][2], xn[2], bw[NBJ][2];
+        };
+        // tile of phase I = t mod 16: ring slot I mod NB, sign buffer (I >> 3) & 1,
         // sign words 2*(I & 7) and 2*(I & 7) + 1 of the super-tile row
-        auto compute = [&](auto ic) {
-            constexpr int I = decltype(ic)::value;
+        auto load = [&](auto ic, Ops& o) {
+            constexpr int I = decltype(ic)::value & 15;
             constexpr int SLOT = (I % NB) * C::kSlot;
             constexpr int WI = 2 * (I & 7);
             constexpr int SBUF = ((I >> 3) & 1) * C::kSBuf;
-            uint2 s2[NA1][FB];
-            u32x4 sb[NA1][FB][2];
 #pragma unroll
             for (int i = 0; i < NA; ++i)
 #pragma unroll
                 for (int b = 0; b < FB; ++b)
-                    s2[i][b] = *reinterpret_cast<const uint2*>(lds + soff[i][WI >> 2] + SBUF + 16 * b * kSRowB + 4 * (WI & 3));
+                    o.s2[i][b] = *reinterpret_cast<const uint2*>(lds + soff[i][WI >> 2] + SBUF + 16 * b * kSRowB + 4 * (WI & 3));
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
-                u32x4 xa[NA1];
 #pragma unroll
-                for (int i = 0; i < NA; ++i) xa[i] = *reinterpret_cast<const u32x4*>(lds + xoff[i][kb] + SLOT);
+                for (int i = 0; i < NA; ++i) o.xa[i][kb] = *reinterpret_cast<const u32x4*>(lds + xoff[i][kb] + SLOT);
                 if (bj[0] >= 0) {
-                    const u32x4 xn = *reinterpret_cast<const u32x4*>(lds + xnoff[kb] + SLOT);
+                    o.xn[kb] = *reinterpret_cast<const u32x4*>(lds + xnoff[kb] + SLOT);
 #pragma unroll
                     for (int j = 0; j < NBJ; ++j)
-                        if (bj[j] >= 0) {
-                            const u32x4 bw = *reinterpret_cast<const u32x4*>(lds + woff[kb] + SLOT + bj[j] * 16 * kRowB);
-                            accn[j] = mfma16<ET>(xn, bw, accn[j]);
-                        }
+                        if (bj[j] >= 0)
+                            o.bw[j][kb] = *reinterpret_cast<const u32x4*>(lds + woff[kb] + SLOT + bj[j] * 16 * kRowB);
                 }
-#pragma unroll
-                for (int b = 0; b < FB; ++b)
-#pragma unroll
-                    for (int i = 0; i < NA; ++i) {
-                        if (kb == 0) decode_signs8x2<ET>(s2[i][b].x, s2[i][b].y, 8 * g, sb[i][b][0], sb[i][b][1]);
-                        accs[i][b] = mfma16<ET>(xa[i], sb[i][b][kb], accs[i][b]);
-                    }
             }
         };
+        auto compute = [&](const Ops& o) {
+#pragma unroll
+            for (int b = 0; b < FB; ++b) {
+                u32x4 sb[NA1][2];
+#pragma unroll
+                for (int i = 0; i < NA; ++i) decode_signs8x2<ET>(o.s2[i][b].x, o.s2[i][b].y, 8 * g, sb[i][0], sb[i][1]);
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < NA; ++i) accs[i][b] = mfma16<ET>(o.xa[i][kb], sb[i][kb], accs[i][b]);
+            }
+            if (bj[0] >= 0)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int j = 0; j < NBJ; ++j)
+                        if (bj[j] >= 0) accn[j] = mfma16<ET>(o.xn[kb], o.bw[j][kb], accn[j]);
+        };
 
-        // ---- main loop, sixteen steps per pass: tile t's copies (and the signs
-        //      it reads) have landed once only the copies of the D-1 later steps
-        //      are in flight ----
+        // ---- main loop, sixteen steps per pass.  Step t issues the copies of
+        //      tile t + D (into the slot of tile t - 1, whose reads completed at
+        //      the previous barrier), waits until tile t + 1 and its signs have
+        //      landed (only the copies of the D - 1 later steps in flight),
+        //      reads tile t + 1's operands, and computes tile t from the
+        //      operands read one step earlier, so their LDS latency overlaps
+        //      the previous step's arithmetic ----
+        Ops oa, ob;
+        wait_vm_lgkm0<(D - 1) * C::ops>();
+        raw_barrier();
+        load(std::integral_constant<int, 0>{}, oa);
         for (int t0 = 0; t0 < KT; t0 += 16) {
             static_for<16>([&](auto ic) {
                 constexpr int I = decltype(ic)::value;
                 const int t = t0 + I;
                 if (t < KT) {
-                    wait_vm_lgkm0<(D - 1) * C::ops>();
-                    raw_barrier();
                     issue_tile(t + D, std::integral_constant<int, (I + D) % NB>{});
                     issue_piece(t, std::integral_constant<int, I & 7>{});
                     __builtin_amdgcn_sched_barrier(0);
-                    compute(ic);
+                    wait_vm_lgkm0<(D - 1) * C::ops>();
+                    raw_barrier();
+                    Ops& cur = (I & 1) ? ob : oa;
+                    Ops& nxt = (I & 1) ? oa : ob;
+                    if (t + 1 < KT) load(std::integral_constant<int, I + 1>{}, nxt);
+                    compute(cur);
                 }
             });
         }
