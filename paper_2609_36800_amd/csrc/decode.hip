@@ -184,10 +184,10 @@ struct StreamCfg {
     static constexpr int kWBytes = kFeat * kTileRow;          // W: 16 rows x 512 B
     static constexpr int kXBytes = XUP ? 0 : XR * kTileRow;   // x: XR rows x 512 B per tile
     static constexpr int kTileBytes = kWBytes + kXBytes;
-    // ring depth (tiles): 6 measured best with x copied per tile (16 rows: 8.77 us
-    // at 4096x4096 against 8.86 for 5 and 9.0 for 4) and level with 8 with x up
-    // front (4, 5 and 10 slower)
-    static constexpr int kNB = 6;
+    // ring depth (tiles): with x copied per tile 5 (16 rows at 4096x4096, medians
+    // of five rounds in one process: 8.42 us against 8.59 for 6, 8.49 for 4 and
+    // 8.75 for 7 or 8); with x up front 6, level with 8 (4, 5 and 10 slower)
+    static constexpr int kNB = XUP ? 6 : 5;
     static constexpr int kRing = kNB * kTileBytes;
     static constexpr int kOpsPerTile = XUP ? 1 : 2;           // copies per wave per tile
     static constexpr int kXLanes = XR * 4;                    // lanes of a wave copying x
