@@ -949,9 +949,22 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(const float* _
                 sum[3] += pc[c][3];
             }
         const int col = n0 + wn * 128 + 32 * j + 8 * q + 4 * (lane >> 5);
+        const size_t at = (size_t)row * N + col;
+        if ((N & 3) == 0 && col + 3 < N) {
+            // four consecutive outputs in one store (col and N multiples of 4)
+            if (y_dtype == kF32) {
+                *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(y) + at) = sum;
+            } else {
+                uint2 v;
+                v.x = cvt_pair<ET>(f32x2v{sum[0], sum[1]});
+                v.y = cvt_pair<ET>(f32x2v{sum[2], sum[3]});
+                *reinterpret_cast<uint2*>(reinterpret_cast<uint16_t*>(y) + at) = v;
+            }
+        } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-            if (col + e < N) store_y<ET>(y, (size_t)row * N + col + e, sum[e], y_dtype);
+            for (int e = 0; e < 4; ++e)
+                if (col + e < N) store_y<ET>(y, at + e, sum[e], y_dtype);
+        }
     }
 }
 
