@@ -110,6 +110,8 @@ MATMUL_CASES = [
     (40, 47, 544, 1, False, AUTO),       # skinny single-tenant kernel
     (40, 100, 512, 5, True, AUTO),       # batched kernel, 8 waves (one round)
     (20, 4100, 256, 5, True, AUTO),      # batched kernel, 4 waves (several rounds)
+    (40, 10000, 640, 6, True, AUTO),     # wide batched kernel, 48 features (ragged last group)
+    (24, 14300, 384, 8, True, AUTO),     # wide batched kernel, 64 features (ragged last group)
     (8, 70, 128, 20, True, AUTO),        # tenant-slot kernel (more than 16 tenants)
     (10, 50, 96, 3, True, AUTO),         # skinny multi-tenant kernel (K not a multiple of 128)
     (300, 520, 576, 1, False, PREFILL),  # fused prefill, streaming
