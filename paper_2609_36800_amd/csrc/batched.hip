@@ -486,6 +486,8 @@ hipError_t launch_et(const uint16_t* x, int M, int K, const uint16_t* w, int N,
 }  // namespace
 
 bool batched_supported(int M, int N, int K, int T) {
+    // Asked only for requests the wide form (wide.hip: 48 or 64 features per
+    // workgroup where those groups fill the CUs) does not take.
     // One round (N <= 4096): the 8-wave kernel for 17 to 64 rows; the
     // tenant-slot kernel (multi.hip, two workgroups per CU) is as fast or
     // faster at 16 rows and below.  Several rounds: every row count from 17,

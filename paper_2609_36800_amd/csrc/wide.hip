@@ -135,7 +135,7 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nl = lane & 15, g = lane >> 4;
     const int n0 = blockIdx.x * NF;
-    const int KT = K / kTK;                                // >= D (host check)
+    const int KT = K / kTK;                                // 2 or more; steps past KT issue only padding copies
     const int KW = K >> 5;
     const char* const hot = reinterpret_cast<const char*>(packed);
 
