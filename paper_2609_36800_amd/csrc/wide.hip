@@ -25,10 +25,11 @@
 //
 // Memory path (8 waves, one workgroup per CU).  K runs in 64-k tiles.  A ring
 // of NB slots holds W (16*FB rows x 128 B) and x (XR rows x 128 B) per tile,
-// issued NB-1 tiles ahead; signs come in 512-k super-tiles (64 B per row),
-// double-buffered, super-tile j+1 issued in pieces during the first steps of
-// super-tile j, early enough that the in-order wait for a tile also covers the
-// signs it reads.  Every wave issues the same number of copies per step (past
+// issued NB tiles ahead with up to 8 sign slots (a slot is refilled as soon as
+// its tile's operands are in registers), NB - 1 with 16; signs come in 512-k
+// super-tiles (64 B per row), double-buffered, super-tile j+1 issued in pieces
+// during the first steps of super-tile j, early enough that the in-order wait
+// for a tile also covers the signs it reads.  Every wave issues the same number of copies per step (past
 // the end of K, or with no real work, a copy of one hot line instead), so one
 // s_waitcnt vmcnt count and one barrier per step hand a tile over.  Operands
 // are read from LDS one step ahead of the arithmetic that uses them.  The loop
@@ -68,7 +69,11 @@ struct WideRouting {
 template <int FB, int XR, int U, int NB>
 struct WideCfg {
     static constexpr int NF = 16 * FB;
-    static constexpr int D = NB - 1;                       // tiles in flight ahead
+    // Tiles issued ahead.  With up to 8 sign slots a slot is refilled as soon
+    // as its tile's operands are in registers (D = NB, 1-3% faster); with 16
+    // the larger sign pieces make the shallower order faster (D = NB - 1, 2%).
+    static constexpr bool kEarly = U <= 8;
+    static constexpr int D = kEarly ? NB : NB - 1;
     static constexpr int kW = NF * kRowB;
     static constexpr int kX = XR * kRowB;
     static constexpr int kSlot = kW + kX;
@@ -89,7 +94,7 @@ struct WideCfg {
     static constexpr int kTotal = kRouteOff + (int)sizeof(WideRouting);
     static_assert(kTotal <= 160 * 1024, "LDS budget");
     static_assert(NB == 2 || NB == 4 || NB == 8, "ring slots: a power of two dividing 8");
-    static_assert(kPieces >= 1, "ring deeper than a super-tile");
+    static_assert(kPieces >= 1 && D >= 2, "ring depth");
     static_assert((kMaxRows + 15 * U) / 16 <= kWaves * FW, "fragments per wave");
     static_assert(NF % kWaves == 0 && XR % kWaves == 0 && kWaves % RB == 0, "copy and base split");
     static_assert((NB - 1) * kSlot + (FB - 1) * 16 * kRowB < 65536, "ring read offsets");
@@ -361,12 +366,16 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
                         if (bj[j] >= 0) accn[j] = mfma16<ET>(o.xn[kb], o.bw[j][kb], accn[j]);
         };
 
-        // ---- main loop, sixteen steps per pass.  Step t issues the copies of
-        //      tile t + D (into the slot of tile t - 1, whose reads completed at
-        //      the previous barrier), waits until tile t + 1 and its signs have
-        //      landed (only the copies of the D - 1 later steps in flight),
-        //      reads tile t + 1's operands, and computes tile t from the
-        //      operands read one step earlier, so their LDS latency overlaps
+        // ---- main loop, sixteen steps per pass.  D = NB: step t waits until
+        //      tile t + 1 and its signs have landed (only the copies of tiles
+        //      t + 2 .. t + D - 1 in flight), then, past the barrier, issues the
+        //      copies of tile t + D into the slot of tile t (whose operands were
+        //      read into registers in the previous step; those reads completed
+        //      before the barrier).  D = NB - 1: step t first issues tile t + D
+        //      into the slot of tile t - 1 (its reads completed at the previous
+        //      barrier), then waits for tile t + 1 the same way.  Either way the
+        //      step then reads tile t + 1's operands and computes tile t from
+        //      the operands read one step earlier, so their LDS latency overlaps
         //      the previous step's arithmetic ----
         Ops oa, ob;
         wait_vm_lgkm0<(D - 1) * C::ops>();
@@ -377,11 +386,17 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
                 constexpr int I = decltype(ic)::value;
                 const int t = t0 + I;
                 if (t < KT) {
+                    if constexpr (C::kEarly) {
+                        wait_vm_lgkm0<(D - 2) * C::ops>();
+                        raw_barrier();
+                    }
                     issue_tile(t + D, std::integral_constant<int, (I + D) % NB>{});
                     issue_piece(t, std::integral_constant<int, I & 7>{});
                     __builtin_amdgcn_sched_barrier(0);
-                    wait_vm_lgkm0<(D - 1) * C::ops>();
-                    raw_barrier();
+                    if constexpr (!C::kEarly) {
+                        wait_vm_lgkm0<(D - 1) * C::ops>();
+                        raw_barrier();
+                    }
                     Ops& cur = (I & 1) ? ob : oa;
                     Ops& nxt = (I & 1) ? oa : ob;
                     if (t + 1 < KT) load(std::integral_constant<int, I + 1>{}, nxt);
