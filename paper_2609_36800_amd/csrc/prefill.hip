@@ -237,9 +237,9 @@ constexpr int kSplitMetaInts = BM + 4;                      // row map, column o
 // kCUs-1 whole (one round), and the L leftover tiles are split along K into
 // S chunks, S = min(8, k-tiles, room / L, kCUs / L): blocks kCUs + l*S + c
 // take chunk c of leftover tile l, so the second round runs on every CU for
-// 1/S of a tile's time.  A chunk's fp32 partial sums go to `part`; the last
-// chunk of a tile to finish (per-tile counter) adds the S partials in chunk
-// order and writes the tile, so the result does not depend on timing.
+// 1/S of a tile's time.  A chunk's fp32 partial sums go to `part`, and the
+// reduction launch that follows adds the S partials of a tile in chunk order
+// and writes its rows, so the result does not depend on timing.
 struct WorkItem {
     int chunk, nchunks, leftover;   // chunk c of nchunks (1: whole tile); leftover tile index
     int nleft;                      // leftover tiles (split ones)
@@ -269,17 +269,37 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
 
     int* h = hist + wv * T;
     for (int i = lane; i < T; i += 64) h[i] = 0;
-    __syncthreads();
-    for (int base = r_beg; base < r_end; base += 512) {
-        int v[8];
+    // the ids of 1024 rows per step, all loads issued together; the first
+    // step's stay in registers for the row collection below
+    constexpr int kIdRegs = 16;
+    auto load_ids = [&](int base, int (&v)[kIdRegs]) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kIdRegs; ++u) {
             const int m = base + 64 * u + lane;
             v[u] = m < r_end ? ids[m] : -1;
         }
+    };
+    // a 64-row run of one id (prompts are runs of rows) is one LDS add, not
+    // 64 adds to one address
+    auto add_hist = [&](const int (&v)[kIdRegs]) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if ((unsigned)v[u] < (unsigned)T) atomicAdd(&h[v[u]], 1);
+        for (int u = 0; u < kIdRegs; ++u) {
+            const int f = __builtin_amdgcn_readfirstlane(v[u]);
+            if (__ballot(v[u] != f) == 0) {
+                if (lane == 0 && (unsigned)f < (unsigned)T) atomicAdd(&h[f], 64);
+            } else if ((unsigned)v[u] < (unsigned)T) {
+                atomicAdd(&h[v[u]], 1);
+            }
+        }
+    };
+    int idr[kIdRegs];
+    load_ids(r_beg, idr);
+    __syncthreads();
+    add_hist(idr);
+    for (int base = r_beg + 64 * kIdRegs; base < r_end; base += 64 * kIdRegs) {
+        int v[kIdRegs];
+        load_ids(base, v);
+        add_hist(v);
     }
     __syncthreads();
 
@@ -308,16 +328,29 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
             for (int kk = 1; kk < kClasses; ++kk) sc[kk] += kk == k;
         }
     }
+    // Inclusive wave scans of the nine counts in four words, interleaved: the
+    // full-tile count alone, the partial-tile class counts three to a word in
+    // 10-bit fields (at most 8 tenants per thread, so at most 512 per wave).
+    static_assert(kMaxGroupedTenants <= 8 * kThreads, "class count fields");
+    int pk[4] = {sc[0], sc[1] | sc[2] << 10 | sc[3] << 20, sc[4] | sc[5] << 10 | sc[6] << 20,
+                 sc[7] | sc[8] << 10};
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int o[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) o[j] = __shfl_up(pk[j], d);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (lane >= d) pk[j] += o[j];
+    }
+    const int inc[kClasses] = {pk[0],
+                               pk[1] & 1023, (pk[1] >> 10) & 1023, pk[1] >> 20,
+                               pk[2] & 1023, (pk[2] >> 10) & 1023, pk[2] >> 20,
+                               pk[3] & 1023, pk[3] >> 10};
 #pragma unroll
     for (int k = 0; k < kClasses; ++k) {
-        int inc = sc[k];
-#pragma unroll
-        for (int d = 1; d < 64; d <<= 1) {
-            const int o = __shfl_up(inc, d);
-            if (lane >= d) inc += o;
-        }
-        if (lane == 63) rows[4 * k + wv] = inc;
-        ex[k] = inc - sc[k];
+        if (lane == 63) rows[4 * k + wv] = inc[k];
+        ex[k] = inc[k] - sc[k];
     }
     __syncthreads();
     int cls_first[kClasses + 1];                 // first row tile of each class
@@ -403,15 +436,9 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
     const int t = info[4], lo = info[5] * BM;
     int rank = 0;
     for (int w2 = 0; w2 < wv; ++w2) rank += hist[w2 * T + t];
-    for (int base = r_beg; base < r_end && rank < lo + BM; base += 512) {
-        int v[8];
+    auto collect = [&](int base, const int (&v)[kIdRegs]) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const int m = base + 64 * u + lane;
-            v[u] = m < r_end ? ids[m] : -1;
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
+        for (int u = 0; u < kIdRegs; ++u) {
             const uint64_t mask = __ballot(v[u] == t);
             if (v[u] == t) {
                 const int below = (int)__builtin_amdgcn_mbcnt_hi(
@@ -421,6 +448,12 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
             }
             rank += __popcll(mask);
         }
+    };
+    if (rank < lo + BM) collect(r_beg, idr);
+    for (int base = r_beg + 64 * kIdRegs; base < r_end && rank < lo + BM; base += 64 * kIdRegs) {
+        int v[kIdRegs];
+        load_ids(base, v);
+        collect(base, v);
     }
     __syncthreads();
     tenant = t;
