@@ -174,8 +174,24 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
         for (int i = 0; i < n; ++i) copy16_to_lds(hot, dummy);
     };
 
-    // ---- routing (wave 0) while the other waves start tile 0 ----
+    // ---- signs: rows are slot-major (row = u*NF + f); copy q of a super-tile
+    //      holds rows 16q .. 16q+15, 4 lanes of 16 B each, and lane l's chunk is
+    //      (l & 3) ^ key64(row) = (l & 3) ^ (l >> 4) ----
+    const int sc4 = 4 * ((lane & 3) ^ (lane >> 4));       // word of the lane's chunk in a super-tile
+    // There are never more tenants than sign slots (T <= U, which the launch
+    // checks), so super-tile 0 holds tenant u in slot u (absent tenants' rows
+    // are copied and never read) and need not wait for the routing; later
+    // super-tiles hold only the tenants present, in the compacted slots the
+    // routing assigns.
+
+    // ---- routing (wave 0) while the other waves start super-tile 0 (tenant u
+    //      in slot u) and tile 0 ----
     if (wv != 0) {
+        for (int q = wv - 1; q < C::nSup; q += kWaves - 1) {
+            const int row = 16 * q + (lane >> 2), u = row / NF, f = row - u * NF;
+            if ((16 * q) / NF < T)
+                copy16_to_lds(packed + ((size_t)u * N + min(n0 + f, N - 1)) * KW + min(sc4, KW - 4), lds + q * 1024);
+        }
         issue_tile(0, std::integral_constant<int, 0>{});
         pads(C::cS);
     } else {
@@ -217,21 +233,25 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
     }
     raw_barrier();
     const int nslot = __builtin_amdgcn_readfirstlane(rt.nslot);
+    const int F = __builtin_amdgcn_readfirstlane(rt.nfrag);
+    // this wave's fragments' alpha, loaded now rather than after the loop (the
+    // loads are older than every tile copy still to come, so the in-order
+    // copy counts below are unaffected)
+    float afr[FW];
+#pragma unroll
+    for (int i = 0; i < FW; ++i) {
+        const int f = wv + kWaves * i;
+        afr[i] = f < F ? alpha[rt.slot_tenant[rt.frag_slot[f]]] : 0.f;
+    }
     if (wv == 0) {
         issue_tile(0, std::integral_constant<int, 0>{});
         pads(C::cS);
     }
 
-    // ---- signs: rows are slot-major (row = u*NF + f); copy q of a super-tile
-    //      holds rows 16q .. 16q+15, 4 lanes of 16 B each, and lane l's chunk is
-    //      (l & 3) ^ key64(row) = (l & 3) ^ (l >> 4) ----
     auto sign_row = [&](int row) {
         const int u = row / NF, f = row - u * NF;
         return packed + ((size_t)rt.slot_tenant[u] * N + min(n0 + f, N - 1)) * KW;
     };
-    const int sc4 = 4 * ((lane & 3) ^ (lane >> 4));       // word of the lane's chunk in a super-tile
-    for (int q = wv; q < C::nSup; q += kWaves)
-        if ((16 * q) / NF < nslot) copy16_to_lds(sign_row(16 * q + (lane >> 2)) + min(sc4, KW - 4), lds + q * 1024);
     const uint32_t* ssrc[C::kPieces * C::cS];
     uint32_t pmask = 0;                                    // piece copies of a present slot
 #pragma unroll
@@ -274,7 +294,6 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
     //      and x*W^T for (row block, feature block) pairs p = fb*RB + rb with
     //      p % 8 == wv, that is row block wv % RB and feature blocks
     //      wv/RB + j*8/RB ----
-    const int F = __builtin_amdgcn_readfirstlane(rt.nfrag);
     const int na = F > wv ? min(FW, (F - wv + kWaves - 1) / kWaves) : 0;
     const int rbw = wv % RB;
     int bj[NBJ];
@@ -295,7 +314,9 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
     auto run = [&](auto nac) {
         constexpr int NA = decltype(nac)::value;
         constexpr int NA1 = NA > 0 ? NA : 1;
-        int xoff[NA1][2], soff[NA1][4];
+        // soff: sign row of the fragment's slot; during super-tile 0 shifted by
+        // sdelta to the row of the tenant itself
+        int xoff[NA1][2], soff[NA1][4], sdelta[NA1];
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int f = wv + kWaves * i;
@@ -304,7 +325,9 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
                 xoff[i][kb] = C::kRingOff + C::kW + r * kRowB + 16 * ((4 * kb + g) ^ key128(r));
-            const int sbase = (rt.frag_slot[f] * NF + nl) * kSRowB;
+            const int slot = rt.frag_slot[f];
+            sdelta[i] = __builtin_amdgcn_readfirstlane((rt.slot_tenant[slot] - slot) * NF * kSRowB);
+            const int sbase = (slot * NF + nl) * kSRowB + sdelta[i];
 #pragma unroll
             for (int q = 0; q < 4; ++q) soff[i][q] = sbase + 16 * (q ^ key64(nl));
         }
@@ -399,6 +422,14 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
                     }
                     Ops& cur = (I & 1) ? ob : oa;
                     Ops& nxt = (I & 1) ? oa : ob;
+                    if constexpr (I == 7) {
+                        // tile 8 starts super-tile 1: compacted slots from here on
+                        if (t0 == 0)
+#pragma unroll
+                            for (int i = 0; i < NA; ++i)
+#pragma unroll
+                                for (int q = 0; q < 4; ++q) soff[i][q] -= sdelta[i];
+                    }
                     if (t + 1 < KT) load(std::integral_constant<int, I + 1>{}, nxt);
                     compute(cur);
                 }
@@ -419,7 +450,7 @@ __global__ __launch_bounds__(kThreads) void wide_batched_kernel(
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int f = wv + kWaves * i;
-            const float a = alpha[rt.slot_tenant[rt.frag_slot[f]]];
+            const float a = afr[i];
 #pragma unroll
             for (int b = 0; b < FB; ++b) {
                 const int n = n0 + 16 * b + nl;
@@ -464,6 +495,7 @@ bool plan_wide(int M, int N, int K, int T, WidePlan* p) {
     const int u = T < M ? T : M;
     if (M < 17 || M > kMaxRows || u > 16 || K < 128 || K % 128 != 0) return false;
     p->u = u <= 8 ? 8 : 16;
+    if (T > p->u) return false;                            // super-tile 0 holds tenant u in slot u
     p->xr = M <= 32 ? 32 : 64;
     const int fg3 = (N + 47) / 48, fg4 = (N + 63) / 64;
     if (fg3 > 5 * kCUs / 8 && fg3 <= kCUs) p->fb = 3;
