@@ -532,6 +532,17 @@ def test_grouped_prefill_tenant_limit():
     assert bd.matmul_path(M, N, K, 2049, True) == SKINNY
 
 
+def test_grouped_prefill_one_row_per_tenant():
+    # 2048 tenants of one row each: every tenant's only tile is a 1-row partial
+    # tile, so each wave's class count reaches its largest value (512 tenants
+    # of one class per wave), the limit of the packed class-count fields
+    M, N, K, T = 2048, 80, 128, 2048
+    p = wl.make_problem(M, N, K, T, seed=28, multi_tenant=True, y_dtype="f32")
+    p.tenant_ids = np.random.default_rng(29).permutation(T).astype(np.int32)
+    log("grouped prefill: 2048 tenants of one row each")
+    check(_grouped(p), oracle_y(p), p.x, p.w, p.alpha, p.tenant_ids)
+
+
 def test_grouped_prefill_deterministic():
     p = wl.make_problem(700, 600, 512, 6, seed=27, multi_tenant=True)
     log("grouped prefill determinism")
