@@ -316,11 +316,18 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
     const int t_beg = min(T, tid * per), t_end = min(T, t_beg + per);
     auto count = [&](int t) { return hist[t] + hist[T + t] + hist[2 * T + t] + hist[3 * T + t]; };
     auto class_of_last = [](int c) { return 1 + (BM - 1 - c % BM) / 32; };   // c % BM != 0
+    // this thread's tenants' row counts, all read at once (at most 8 tenants)
+    constexpr int kPer = kMaxGroupedTenants / kThreads;
+    static_assert(kPer * kThreads == kMaxGroupedTenants && kPer <= 8, "tenants per thread");
+    int cnt[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) cnt[i] = t_beg + i < t_end ? count(t_beg + i) : 0;
     int sc[kClasses], ex[kClasses];
 #pragma unroll
     for (int k = 0; k < kClasses; ++k) sc[k] = 0;
-    for (int t = t_beg; t < t_end; ++t) {
-        const int c = count(t);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+        const int c = cnt[i];
         sc[0] += c / BM;
         if (c % BM != 0) {
             const int k = class_of_last(c);
@@ -353,12 +360,20 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
         ex[k] = inc[k] - sc[k];
     }
     __syncthreads();
+    // the four waves' class totals, all read at once, then combined without
+    // branches: class starts, and this wave's offset within each class
+    static_assert(kThreads == 4 * 64, "four waves");
+    int wtot[kClasses][4];
+#pragma unroll
+    for (int k = 0; k < kClasses; ++k)
+#pragma unroll
+        for (int w2 = 0; w2 < 4; ++w2) wtot[k][w2] = rows[4 * k + w2];
     int cls_first[kClasses + 1];                 // first row tile of each class
     cls_first[0] = 0;
 #pragma unroll
     for (int k = 0; k < kClasses; ++k) {
-        cls_first[k + 1] = cls_first[k] + rows[4 * k] + rows[4 * k + 1] + rows[4 * k + 2] + rows[4 * k + 3];
-        for (int w2 = 0; w2 < wv; ++w2) ex[k] += rows[4 * k + w2];
+        cls_first[k + 1] = cls_first[k] + wtot[k][0] + wtot[k][1] + wtot[k][2] + wtot[k][3];
+        ex[k] += (wv > 0 ? wtot[k][0] : 0) + (wv > 1 ? wtot[k][1] : 0) + (wv > 2 ? wtot[k][2] : 0);
     }
     const int total = cls_first[kClasses];
     __syncthreads();            // the totals are read before info[4..5] and rows[] are reused
@@ -408,8 +423,11 @@ __device__ bool route_rows(const int32_t* __restrict__ ids, int M, int T, int ti
         }
     if (pv >= exk && pv < exk + sck) {
         int first = exk;
-        for (int t = t_beg; t < t_end; ++t) {
-            const int c = count(t);
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int t = t_beg + i;
+            if (t >= t_end) break;
+            const int c = cnt[i];
             if (k == 0) {
                 const int nf = c / BM;
                 if (pv < first + nf) {
