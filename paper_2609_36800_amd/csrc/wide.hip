@@ -15,8 +15,10 @@
 // (rows/16 with 16 features).
 //
 // Routing.  Wave 0 sorts the rows by tenant (ballots) into fragments of up to
-// 16 rows of one tenant; sign slot u holds the u-th tenant present, so only
-// present tenants' signs are copied.  Wave w computes the sign products of
+// 16 rows of one tenant; past the first 512-k super-tile, sign slot u holds the
+// u-th tenant present, so only present tenants' signs are copied (the first
+// super-tile holds tenant u in slot u and is copied while wave 0 routes).
+// Wave w computes the sign products of
 // fragments w, w+8, w+16 against all 16*FB features (per 32-k block one x
 // read, FB sign decodes and FB MFMAs) and x*W^T on the rows in their own order
 // for its share of the (16-row block, 16-feature block) pairs (one MFMA per 16
@@ -29,9 +31,10 @@
 // its tile's operands are in registers), NB - 1 with 16; signs come in 512-k
 // super-tiles (64 B per row), double-buffered, super-tile j+1 issued in pieces
 // during the first steps of super-tile j, early enough that the in-order wait
-// for a tile also covers the signs it reads.  Every wave issues the same number of copies per step (past
-// the end of K, or with no real work, a copy of one hot line instead), so one
-// s_waitcnt vmcnt count and one barrier per step hand a tile over.  Operands
+// for a tile also covers the signs it reads.  Every wave issues the same
+// number of copies per step (past the end of K, or with no real work, a copy
+// of one hot line instead), so one s_waitcnt vmcnt count and one barrier per
+// step hand a tile over.  Operands
 // are read from LDS one step ahead of the arithmetic that uses them.  The loop
 // runs sixteen steps per pass, so ring slots, super-tile phases and sign words
 // are compile-time offsets of the LDS reads.
