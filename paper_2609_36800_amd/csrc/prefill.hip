@@ -980,24 +980,36 @@ __global__ __launch_bounds__(kThreads) void prefill_reduce_kernel(const float* _
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int wm = wv >> 1, wn = wv & 1;
     const f32x4* all = reinterpret_cast<const f32x4*>(part) + (size_t)l * S * kSplitVecs * kThreads;
+    // every load of the block's vectors (all chunks) is issued before the
+    // first add, so their latencies overlap
+    int rows[kPerBlock];
+#pragma unroll
+    for (int vv = 0; vv < kPerBlock; ++vv) {
+        const int v = vb * kPerBlock + vv;
+        rows[vv] = meta[wm * 128 + 32 * (v >> 4) + (lane & 31)];
+    }
+    f32x4 pc[kPerBlock][8];
+#pragma unroll
+    for (int vv = 0; vv < kPerBlock; ++vv) {
+        const int v = vb * kPerBlock + vv;
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+            if (rows[vv] >= 0 && c < S) pc[vv][c] = all[((size_t)c * kSplitVecs + v) * kThreads + tid];
+    }
 #pragma unroll
     for (int vv = 0; vv < kPerBlock; ++vv) {
         const int v = vb * kPerBlock + vv;              // (i * 4 + j) * 4 + q
-        const int i = v >> 4, j = (v >> 2) & 3, q = v & 3;
-        const int row = meta[wm * 128 + 32 * i + (lane & 31)];
+        const int j = (v >> 2) & 3, q = v & 3;
+        const int row = rows[vv];
         if (row < 0) continue;
-        f32x4 pc[8];
-#pragma unroll
-        for (int c = 0; c < 8; ++c)
-            if (c < S) pc[c] = all[((size_t)c * kSplitVecs + v) * kThreads + tid];
-        f32x4 sum = pc[0];
+        f32x4 sum = pc[vv][0];
 #pragma unroll
         for (int c = 1; c < 8; ++c)
             if (c < S) {
-                sum[0] += pc[c][0];
-                sum[1] += pc[c][1];
-                sum[2] += pc[c][2];
-                sum[3] += pc[c][3];
+                sum[0] += pc[vv][c][0];
+                sum[1] += pc[vv][c][1];
+                sum[2] += pc[vv][c][2];
+                sum[3] += pc[vv][c][3];
             }
         const int col = n0 + wn * 128 + 32 * j + 8 * q + 4 * (lane >> 5);
         const size_t at = (size_t)row * N + col;
